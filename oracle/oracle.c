@@ -1,0 +1,676 @@
+/*
+ * oracle.c -- plain CPU oracle (test infrastructure only; see oracle.h).
+ *
+ * Written for clarity, not speed: sorted arrays, binary search, recursion
+ * over the query's computation plan.  Every function names the passage of
+ * the paper it follows.  Points the paper leaves open are taken as:
+ *   - root of reverse sampling uniform over entities with an in-edge;
+ *   - each projection step picks an in-relation uniformly among the
+ *     entity's distinct in-relations, then an in-neighbour uniformly;
+ *   - union branches are grounded from the same entity as intersection
+ *     branches;
+ *   - an attempt is rejected when a walk reaches an entity without
+ *     in-edges, when two single-projection sibling branches get the same
+ *     (anchor, relation), or when max_fanout > 0 and a grounded step's
+ *     forward neighbour list under its relation exceeds max_fanout;
+ *   - candidates are uniform over all V entities, kept iff outside A_q and
+ *     not drawn before (the negative set is a set).
+ */
+#include "oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+#include <omp.h>
+
+/* ------------------------------------------------------------------ Philox */
+/* Philox4x32-10, Salmon et al., "Parallel Random Numbers: As Easy as 1, 2, 3",
+   SC'11: ten rounds of two 32x32->64 multiplies with a Weyl key schedule. */
+void oracle_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; round++) {
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+uint64_t oracle_pick(uint64_t u, uint64_t n)
+{
+    return (uint64_t)(((unsigned __int128)u * n) >> 64);
+}
+
+uint64_t oracle_draw(uint64_t seed, uint32_t tag, uint32_t qid, uint32_t t, uint32_t j)
+{
+    uint32_t ctr[4] = {j, t, qid, tag};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t x[4];
+    oracle_philox(ctr, key, x);
+    return ((uint64_t)x[1] << 32) | x[0];
+}
+
+#define TAG_POS 1u
+#define TAG_NEG 2u
+
+/* ------------------------------------------------------------------- graph */
+/* The KG is a set of triples (Sec. 2); A_r(v) is the set of tails of v under
+   r (appendix on the query computation plan).  Forward edges are kept sorted
+   by (head, relation, tail) and reverse edges by (tail, relation, head). */
+struct okg {
+    int32_t V, R;
+    int64_t E;
+    int64_t *f_off;             /* [V+1] */
+    int32_t *f_rel, *f_nbr;     /* [E] */
+    int64_t *r_off;             /* [V+1] */
+    int32_t *r_rel, *r_nbr;     /* [E] */
+    int64_t *rs_off;            /* [V+1] first reverse segment of each entity */
+    int32_t *rs_rel;            /* [S_rev] */
+    int64_t *rs_beg;            /* [S_rev+1] edge range of each reverse segment */
+    int64_t S_fwd, S_rev;
+    int32_t *active_in;
+    int64_t n_active;
+};
+
+static int cmp_u64(const void *a, const void *b)
+{
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return x < y ? -1 : x > y;
+}
+
+static int cmp_i32(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return x < y ? -1 : x > y;
+}
+
+/* Group edges by a primary entity, sort each group by (relation, other end),
+   drop duplicates.  prim/rel/oth give edge i. */
+typedef void (*edge_fn)(const void *ctx, int64_t i, int32_t *p, int32_t *r, int32_t *o);
+
+static int group_sort(const void *ctx, edge_fn edge, int64_t n, int32_t V, int nthreads,
+                      int64_t **off_out, int32_t **rel_out, int32_t **nbr_out, int64_t *m_out)
+{
+    int64_t *off = (int64_t *)calloc((size_t)V + 1, sizeof(int64_t));
+    int64_t *cur = (int64_t *)malloc(((size_t)V + 1) * sizeof(int64_t));
+    uint64_t *key = (uint64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(uint64_t));
+    if (!off || !cur || !key) { free(off); free(cur); free(key); return -1; }
+    for (int64_t i = 0; i < n; i++) {
+        int32_t p, r, o;
+        edge(ctx, i, &p, &r, &o);
+        off[p + 1]++;
+    }
+    for (int32_t v = 0; v < V; v++) off[v + 1] += off[v];
+    memcpy(cur, off, ((size_t)V + 1) * sizeof(int64_t));
+    for (int64_t i = 0; i < n; i++) {
+        int32_t p, r, o;
+        edge(ctx, i, &p, &r, &o);
+        key[cur[p]++] = ((uint64_t)(uint32_t)r << 32) | (uint32_t)o;
+    }
+#pragma omp parallel for schedule(dynamic, 1024) num_threads(nthreads)
+    for (int32_t v = 0; v < V; v++)
+        if (off[v + 1] - off[v] > 1) qsort(key + off[v], (size_t)(off[v + 1] - off[v]), 8, cmp_u64);
+    /* remove duplicates inside each group */
+    int64_t w = 0;
+    for (int32_t v = 0; v < V; v++) {
+        int64_t b = off[v], e = off[v + 1];
+        cur[v] = w;
+        for (int64_t k = b; k < e; k++)
+            if (k == b || key[k] != key[k - 1]) key[w++] = key[k];
+    }
+    cur[V] = w;
+    int32_t *rel = (int32_t *)malloc((size_t)(w > 0 ? w : 1) * 4);
+    int32_t *nbr = (int32_t *)malloc((size_t)(w > 0 ? w : 1) * 4);
+    if (!rel || !nbr) { free(off); free(cur); free(key); free(rel); free(nbr); return -1; }
+    for (int64_t k = 0; k < w; k++) {
+        rel[k] = (int32_t)(key[k] >> 32);
+        nbr[k] = (int32_t)(uint32_t)key[k];
+    }
+    free(key);
+    free(off);
+    *off_out = cur;
+    *rel_out = rel;
+    *nbr_out = nbr;
+    *m_out = w;
+    return 0;
+}
+
+typedef struct { const int32_t *tr; int64_t n; int32_t R; } in_ctx;
+
+/* input triple i, or for i >= n the inverse (t, r+R, h) of triple i-n */
+static void in_edge(const void *c, int64_t i, int32_t *p, int32_t *r, int32_t *o)
+{
+    const in_ctx *x = (const in_ctx *)c;
+    if (i < x->n) { *p = x->tr[3 * i]; *r = x->tr[3 * i + 1]; *o = x->tr[3 * i + 2]; }
+    else { i -= x->n; *p = x->tr[3 * i + 2]; *r = x->tr[3 * i + 1] + x->R; *o = x->tr[3 * i]; }
+}
+
+typedef struct { const okg *g; const int32_t *head; } fwd_ctx;
+
+/* forward edge i seen from its tail: (tail, relation, head) */
+static void rev_edge(const void *c, int64_t i, int32_t *p, int32_t *r, int32_t *o)
+{
+    const fwd_ctx *x = (const fwd_ctx *)c;
+    *p = x->g->f_nbr[i];
+    *r = x->g->f_rel[i];
+    *o = x->head[i];
+}
+
+void oracle_graph_free(okg *g)
+{
+    if (!g) return;
+    free(g->f_off); free(g->f_rel); free(g->f_nbr);
+    free(g->r_off); free(g->r_rel); free(g->r_nbr);
+    free(g->rs_off); free(g->rs_rel); free(g->rs_beg);
+    free(g->active_in);
+    free(g);
+}
+
+okg *oracle_graph_build(const int32_t *triples, int64_t n, int32_t V, int32_t R, int add_inverse,
+                        int nthreads)
+{
+    if (V <= 0 || R <= 0 || n < 0 || (n > 0 && !triples)) return NULL;
+    if (add_inverse && (int64_t)R * 2 > 0x7FFFFFFF) return NULL;
+    for (int64_t i = 0; i < n; i++) {
+        int32_t h = triples[3 * i], r = triples[3 * i + 1], t = triples[3 * i + 2];
+        if (h < 0 || h >= V || t < 0 || t >= V || r < 0 || r >= R) return NULL;
+    }
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+    okg *g = (okg *)calloc(1, sizeof(okg));
+    if (!g) return NULL;
+    g->V = V;
+    g->R = add_inverse ? 2 * R : R;
+    in_ctx ic = {triples, n, R};
+    int64_t m;
+    if (group_sort(&ic, in_edge, add_inverse ? 2 * n : n, V, nthreads, &g->f_off, &g->f_rel,
+                   &g->f_nbr, &m)) { oracle_graph_free(g); return NULL; }
+    g->E = m;
+    /* head of every forward edge, for building the reverse lists */
+    int32_t *head = (int32_t *)malloc((size_t)(m > 0 ? m : 1) * 4);
+    if (!head) { oracle_graph_free(g); return NULL; }
+    for (int32_t v = 0; v < V; v++)
+        for (int64_t k = g->f_off[v]; k < g->f_off[v + 1]; k++) head[k] = v;
+    fwd_ctx fc = {g, head};
+    int64_t m2;
+    int rc = group_sort(&fc, rev_edge, m, V, nthreads, &g->r_off, &g->r_rel, &g->r_nbr, &m2);
+    free(head);
+    if (rc || m2 != m) { oracle_graph_free(g); return NULL; }
+    /* forward segment count; reverse segments (runs of one relation) */
+    g->S_fwd = 0;
+    for (int32_t v = 0; v < V; v++)
+        for (int64_t k = g->f_off[v]; k < g->f_off[v + 1]; k++)
+            if (k == g->f_off[v] || g->f_rel[k] != g->f_rel[k - 1]) g->S_fwd++;
+    int64_t S = 0;
+    for (int32_t v = 0; v < V; v++)
+        for (int64_t k = g->r_off[v]; k < g->r_off[v + 1]; k++)
+            if (k == g->r_off[v] || g->r_rel[k] != g->r_rel[k - 1]) S++;
+    g->S_rev = S;
+    g->rs_off = (int64_t *)malloc(((size_t)V + 1) * 8);
+    g->rs_rel = (int32_t *)malloc((size_t)(S > 0 ? S : 1) * 4);
+    g->rs_beg = (int64_t *)malloc(((size_t)S + 1) * 8);
+    if (!g->rs_off || !g->rs_rel || !g->rs_beg) { oracle_graph_free(g); return NULL; }
+    S = 0;
+    for (int32_t v = 0; v < V; v++) {
+        g->rs_off[v] = S;
+        for (int64_t k = g->r_off[v]; k < g->r_off[v + 1]; k++)
+            if (k == g->r_off[v] || g->r_rel[k] != g->r_rel[k - 1]) {
+                g->rs_rel[S] = g->r_rel[k];
+                g->rs_beg[S] = k;
+                S++;
+            }
+    }
+    g->rs_off[V] = S;
+    g->rs_beg[S] = m;
+    int64_t na = 0;
+    for (int32_t v = 0; v < V; v++) na += g->r_off[v + 1] > g->r_off[v];
+    g->active_in = (int32_t *)malloc((size_t)(na > 0 ? na : 1) * 4);
+    if (!g->active_in) { oracle_graph_free(g); return NULL; }
+    na = 0;
+    for (int32_t v = 0; v < V; v++)
+        if (g->r_off[v + 1] > g->r_off[v]) g->active_in[na++] = v;
+    g->n_active = na;
+    return g;
+}
+
+void oracle_graph_stats(const okg *g, int64_t *st)
+{
+    int64_t mo = 0, mi = 0, ms = 0;
+    for (int32_t v = 0; v < g->V; v++) {
+        if (g->f_off[v + 1] - g->f_off[v] > mo) mo = g->f_off[v + 1] - g->f_off[v];
+        if (g->r_off[v + 1] - g->r_off[v] > mi) mi = g->r_off[v + 1] - g->r_off[v];
+    }
+    for (int64_t s = 0; s < g->S_rev; s++)
+        if (g->rs_beg[s + 1] - g->rs_beg[s] > ms) ms = g->rs_beg[s + 1] - g->rs_beg[s];
+    st[0] = g->V; st[1] = g->R; st[2] = g->E; st[3] = g->S_fwd; st[4] = g->S_rev;
+    st[5] = g->n_active; st[6] = mo; st[7] = mi; st[8] = ms;
+}
+
+int64_t oracle_graph_edges(const okg *g, int dir, int32_t v, int32_t *rel, int32_t *nbr)
+{
+    if (v < 0 || v >= g->V) return -1;
+    const int64_t *off = dir ? g->r_off : g->f_off;
+    const int32_t *r = dir ? g->r_rel : g->f_rel, *o = dir ? g->r_nbr : g->f_nbr;
+    int64_t b = off[v], e = off[v + 1];
+    if (rel) memcpy(rel, r + b, (size_t)(e - b) * 4);
+    if (nbr) memcpy(nbr, o + b, (size_t)(e - b) * 4);
+    return e - b;
+}
+
+int64_t oracle_graph_active_in(const okg *g, int32_t *out)
+{
+    if (out) memcpy(out, g->active_in, (size_t)g->n_active * 4);
+    return g->n_active;
+}
+
+/* [*b, *e): the edges of v under relation r in one direction (binary search
+   for the run of relation r inside v's sorted edge list). */
+static void rel_range(const int64_t *off, const int32_t *rel, int32_t v, int32_t r, int64_t *b,
+                      int64_t *e)
+{
+    int64_t lo = off[v], hi = off[v + 1];
+    while (lo < hi) {               /* first edge with relation >= r */
+        int64_t mid = lo + (hi - lo) / 2;
+        if (rel[mid] < r) lo = mid + 1; else hi = mid;
+    }
+    int64_t first = lo;
+    hi = off[v + 1];
+    while (lo < hi) {               /* first edge with relation > r */
+        int64_t mid = lo + (hi - lo) / 2;
+        if (rel[mid] <= r) lo = mid + 1; else hi = mid;
+    }
+    *b = first;
+    *e = lo;
+}
+
+/* ---------------------------------------------------------- query plans */
+/* Computation plans of the nine negation-free structures (Sec. 2, "Query
+   computation plan"; appendix on the computation plan).  Nodes are listed
+   children first.  Projection nodes carry a relation slot, anchors an
+   anchor slot; intersection and union edges carry no relation. */
+enum { N_ANCHOR = 0, N_PROJ = 1, N_AND = 2, N_OR = 3 };
+typedef struct { int op, nch, ch[3], slot; } onode;
+typedef struct { const char *name; int n, root; onode nd[8]; } otype;
+
+#define A(s)       {N_ANCHOR, 0, {-1, -1, -1}, s}
+#define P(c, s)    {N_PROJ, 1, {c, -1, -1}, s}
+#define AND2(a, b) {N_AND, 2, {a, b, -1}, -1}
+#define AND3(a, b, c) {N_AND, 3, {a, b, c}, -1}
+#define OR2(a, b)  {N_OR, 2, {a, b, -1}, -1}
+
+static const otype TYPES[9] = {
+    {"1p", 2, 1, {A(0), P(0, 0)}},
+    {"2p", 3, 2, {A(0), P(0, 0), P(1, 1)}},
+    {"3p", 4, 3, {A(0), P(0, 0), P(1, 1), P(2, 2)}},
+    {"2i", 5, 4, {A(0), P(0, 0), A(1), P(2, 1), AND2(1, 3)}},
+    {"3i", 7, 6, {A(0), P(0, 0), A(1), P(2, 1), A(2), P(4, 2), AND3(1, 3, 5)}},
+    {"ip", 6, 5, {A(0), P(0, 0), A(1), P(2, 1), AND2(1, 3), P(4, 2)}},
+    {"pi", 6, 5, {A(0), P(0, 0), P(1, 1), A(1), P(3, 2), AND2(2, 4)}},
+    {"2u", 5, 4, {A(0), P(0, 0), A(1), P(2, 1), OR2(1, 3)}},
+    {"up", 6, 5, {A(0), P(0, 0), A(1), P(2, 1), OR2(1, 3), P(4, 2)}},
+};
+
+int oracle_type_id(const char *name)
+{
+    for (int k = 0; k < 9; k++)
+        if (strcmp(TYPES[k].name, name) == 0) return k;
+    return -1;
+}
+
+int oracle_type_plan(int qtype, int32_t *op, int32_t *child, int32_t *slot, int32_t *root)
+{
+    if (qtype < 0 || qtype > 8) return -1;
+    const otype *T = &TYPES[qtype];
+    for (int k = 0; k < T->n; k++) {
+        op[k] = T->nd[k].op;
+        slot[k] = T->nd[k].slot;
+        for (int c = 0; c < 3; c++) child[3 * k + c] = c < T->nd[k].nch ? T->nd[k].ch[c] : -1;
+    }
+    *root = T->root;
+    return T->n;
+}
+
+/* ------------------------------------------------------------ entity sets */
+typedef struct { int32_t *v; int64_t n; } iset;
+
+static int proj_mode = 0;   /* 0: auto, 1: always sort, 2: always bitmap (for tests) */
+void oracle_set_proj_mode(int mode) { proj_mode = mode; }
+
+/* Relation projection: union of A_r(v) over v in S, as a sorted set. */
+static iset set_proj(const okg *g, iset S, int32_t r)
+{
+    int64_t total = 0;
+    for (int64_t i = 0; i < S.n; i++) {
+        int64_t b, e;
+        rel_range(g->f_off, g->f_rel, S.v[i], r, &b, &e);
+        total += e - b;
+    }
+    iset out = {NULL, 0};
+    if (total == 0) return out;
+    int use_bitmap = proj_mode == 2 || (proj_mode == 0 && total * 16 >= g->V);
+    if (use_bitmap) {
+        int64_t words = ((int64_t)g->V + 63) / 64;
+        uint64_t *bits = (uint64_t *)calloc((size_t)words, 8);
+        for (int64_t i = 0; i < S.n; i++) {
+            int64_t b, e;
+            rel_range(g->f_off, g->f_rel, S.v[i], r, &b, &e);
+            for (int64_t k = b; k < e; k++) bits[g->f_nbr[k] >> 6] |= 1ULL << (g->f_nbr[k] & 63);
+        }
+        int64_t cnt = 0;
+        for (int64_t w = 0; w < words; w++) cnt += __builtin_popcountll(bits[w]);
+        out.v = (int32_t *)malloc((size_t)cnt * 4);
+        for (int64_t w = 0; w < words; w++)
+            for (uint64_t x = bits[w]; x; x &= x - 1) out.v[out.n++] = (int32_t)(w * 64 + __builtin_ctzll(x));
+        free(bits);
+    } else {
+        out.v = (int32_t *)malloc((size_t)total * 4);
+        for (int64_t i = 0; i < S.n; i++) {
+            int64_t b, e;
+            rel_range(g->f_off, g->f_rel, S.v[i], r, &b, &e);
+            for (int64_t k = b; k < e; k++) out.v[out.n++] = g->f_nbr[k];
+        }
+        qsort(out.v, (size_t)out.n, 4, cmp_i32);
+        int64_t w = 0;
+        for (int64_t k = 0; k < out.n; k++)
+            if (k == 0 || out.v[k] != out.v[k - 1]) out.v[w++] = out.v[k];
+        out.n = w;
+    }
+    return out;
+}
+
+/* Intersection / union of two sorted sets by a linear merge (the appendix on
+   the optimal cut notes sorted lists make both linear time). */
+static iset set_merge(iset a, iset b, int is_union)
+{
+    iset o;
+    o.v = (int32_t *)malloc((size_t)(a.n + b.n > 0 ? a.n + b.n : 1) * 4);
+    o.n = 0;
+    int64_t i = 0, j = 0;
+    while (i < a.n && j < b.n) {
+        if (a.v[i] < b.v[j]) { if (is_union) o.v[o.n++] = a.v[i]; i++; }
+        else if (a.v[i] > b.v[j]) { if (is_union) o.v[o.n++] = b.v[j]; j++; }
+        else { o.v[o.n++] = a.v[i]; i++; j++; }
+    }
+    if (is_union) {
+        while (i < a.n) o.v[o.n++] = a.v[i++];
+        while (j < b.n) o.v[o.n++] = b.v[j++];
+    }
+    return o;
+}
+
+static int set_has(iset s, int32_t x)
+{
+    int64_t lo = 0, hi = s.n;
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (s.v[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo < s.n && s.v[lo] == x;
+}
+
+/* Exhaustive execution of the plan from the anchors to node k (Sec. 2,
+   "Traversing the KG using the computation plan to find answers"). */
+static iset eval_node(const okg *g, const otype *T, int k, const int32_t *anchors,
+                      const int32_t *relations)
+{
+    const onode *nd = &T->nd[k];
+    iset out = {NULL, 0};
+    if (nd->op == N_ANCHOR) {
+        out.v = (int32_t *)malloc(4);
+        out.v[0] = anchors[nd->slot];
+        out.n = 1;
+    } else if (nd->op == N_PROJ) {
+        iset in = eval_node(g, T, nd->ch[0], anchors, relations);
+        out = set_proj(g, in, relations[nd->slot]);
+        free(in.v);
+    } else {
+        out = eval_node(g, T, nd->ch[0], anchors, relations);
+        for (int c = 1; c < nd->nch; c++) {
+            iset b = eval_node(g, T, nd->ch[c], anchors, relations);
+            iset m = set_merge(out, b, nd->op == N_OR);
+            free(out.v);
+            free(b.v);
+            out = m;
+        }
+    }
+    return out;
+}
+
+int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
+                          const int32_t *relations, int32_t *out, int64_t cap)
+{
+    if (qtype < 0 || qtype > 8) return -1;
+    const otype *T = &TYPES[qtype];
+    for (int k = 0; k < T->n; k++) {
+        const onode *nd = &T->nd[k];
+        if (nd->op == N_ANCHOR && (anchors[nd->slot] < 0 || anchors[nd->slot] >= g->V)) return -1;
+        if (nd->op == N_PROJ && (relations[nd->slot] < 0 || relations[nd->slot] >= g->R)) return -1;
+    }
+    iset s = eval_node(g, T, T->root, anchors, relations);
+    if (out) memcpy(out, s.v, (size_t)(s.n < cap ? s.n : cap) * 4);
+    int64_t n = s.n;
+    free(s.v);
+    return n;
+}
+
+/* ----------------------------------------------------- reverse sampling */
+/* Reverse directional sampling (Sec. 3.1; appendix on reverse directional
+   sampling): depth-first from the root to the anchors, children in index
+   order.  A projection node whose output entity is e grounds its relation
+   and input entity by g(e): an in-relation of e, then an in-neighbour of e
+   under it.  Intersection and union children take the node's own entity. */
+typedef struct {
+    const okg *g;
+    uint64_t seed;
+    uint32_t qid, t, j;
+    int32_t max_fanout;
+    int32_t anchors[3], relations[3];
+} walk;
+
+static int ground(walk *w, const otype *T, int k, int32_t e)
+{
+    const onode *nd = &T->nd[k];
+    const okg *g = w->g;
+    if (nd->op == N_ANCHOR) {
+        w->anchors[nd->slot] = e;
+        return 1;
+    }
+    if (nd->op == N_PROJ) {
+        int64_t nseg = g->rs_off[e + 1] - g->rs_off[e];
+        uint64_t u0 = oracle_draw(w->seed, TAG_POS, w->qid, w->t, w->j);
+        uint64_t u1 = oracle_draw(w->seed, TAG_POS, w->qid, w->t, w->j + 1);
+        w->j += 2;
+        if (nseg == 0) return 0;                         /* no in-edge: reject */
+        int64_t s = g->rs_off[e] + (int64_t)oracle_pick(u0, (uint64_t)nseg);
+        int64_t len = g->rs_beg[s + 1] - g->rs_beg[s];
+        int32_t x = g->r_nbr[g->rs_beg[s] + (int64_t)oracle_pick(u1, (uint64_t)len)];
+        int32_t r = g->rs_rel[s];
+        if (w->max_fanout > 0) {
+            int64_t b, en;
+            rel_range(g->f_off, g->f_rel, x, r, &b, &en);
+            if (en - b > w->max_fanout) return 0;         /* step expands too much */
+        }
+        w->relations[nd->slot] = r;
+        return ground(w, T, nd->ch[0], x);
+    }
+    for (int c = 0; c < nd->nch; c++)
+        if (!ground(w, T, nd->ch[c], e)) return 0;
+    /* two single-projection branches grounded to the same (anchor, relation)
+       make a degenerate intersection or union: reject */
+    for (int a = 0; a < nd->nch; a++)
+        for (int b = a + 1; b < nd->nch; b++) {
+            const onode *x = &T->nd[nd->ch[a]], *y = &T->nd[nd->ch[b]];
+            if (x->op != N_PROJ || y->op != N_PROJ) continue;
+            const onode *xa = &T->nd[x->ch[0]], *ya = &T->nd[y->ch[0]];
+            if (xa->op != N_ANCHOR || ya->op != N_ANCHOR) continue;
+            if (w->anchors[xa->slot] == w->anchors[ya->slot] &&
+                w->relations[x->slot] == w->relations[y->slot]) return 0;
+        }
+    return 1;
+}
+
+/* small open-addressing set of candidate ids (first-occurrence test) */
+typedef struct { int32_t *slot; uint32_t mask; } hset;
+
+static int hset_insert(hset *h, int32_t x)   /* 1 if newly inserted */
+{
+    uint32_t i = ((uint32_t)x * 0x9E3779B1u) & h->mask;
+    while (h->slot[i] != -1) {
+        if (h->slot[i] == x) return 0;
+        i = (i + 1) & h->mask;
+    }
+    h->slot[i] = x;
+    return 1;
+}
+
+static void sample_one(const okg *g, const otype *T, const oracle_args *a, int64_t b,
+                       int32_t *anchors, int32_t *relations, int32_t *positive, int32_t *negatives,
+                       int32_t *n_valid, int32_t *pos_attempts, int32_t *neg_draws)
+{
+    uint32_t qid = (uint32_t)(a->query_offset + (uint64_t)b);
+    for (int k = 0; k < 3; k++) { anchors[3 * b + k] = -1; relations[3 * b + k] = -1; }
+    for (int k = 0; k < a->n_neg; k++) negatives[(int64_t)a->n_neg * b + k] = -1;
+    positive[b] = -1;
+    /* positive: first accepted attempt */
+    int found = 0;
+    walk w;
+    int32_t root = -1;
+    uint32_t t;
+    for (t = 0; t < (uint32_t)a->pos_tries && !found; t++) {
+        w.g = g; w.seed = a->seed; w.qid = qid; w.t = t; w.j = 1; w.max_fanout = a->max_fanout;
+        for (int k = 0; k < 3; k++) { w.anchors[k] = -1; w.relations[k] = -1; }
+        if (g->n_active == 0) continue;
+        uint64_t u = oracle_draw(a->seed, TAG_POS, qid, t, 0);
+        root = g->active_in[oracle_pick(u, (uint64_t)g->n_active)];
+        found = ground(&w, T, T->root, root);
+    }
+    if (!found) {
+        n_valid[b] = -1;
+        pos_attempts[b] = a->pos_tries;
+        neg_draws[b] = -1;
+        return;
+    }
+    pos_attempts[b] = (int32_t)t;   /* t was incremented past the accepted attempt */
+    positive[b] = root;
+    for (int k = 0; k < 3; k++) { anchors[3 * b + k] = w.anchors[k]; relations[3 * b + k] = w.relations[k]; }
+    /* negatives: rejection sampling against the full answer set */
+    iset Aq = eval_node(g, T, T->root, w.anchors, w.relations);
+    uint32_t cap = 16;
+    while (cap < 2u * (uint32_t)a->neg_tries) cap <<= 1;
+    hset seen = {(int32_t *)malloc((size_t)cap * 4), cap - 1};
+    memset(seen.slot, 0xFF, (size_t)cap * 4);
+    int32_t acc = 0, draws = a->neg_tries;
+    if (a->n_neg == 0) draws = 0;
+    for (int32_t j = 0; j < a->neg_tries && acc < a->n_neg; j++) {
+        uint64_t u = oracle_draw(a->seed, TAG_NEG, qid, 0, (uint32_t)j);
+        int32_t c = (int32_t)oracle_pick(u, (uint64_t)g->V);
+        int first = hset_insert(&seen, c);
+        if (first && !set_has(Aq, c)) {
+            negatives[(int64_t)a->n_neg * b + acc] = c;
+            acc++;
+            if (acc == a->n_neg) draws = j + 1;
+        }
+    }
+    n_valid[b] = acc;
+    neg_draws[b] = draws;
+    free(seen.slot);
+    free(Aq.v);
+}
+
+int oracle_sample(const okg *g, int qtype, const oracle_args *a, int32_t *anchors,
+                  int32_t *relations, int32_t *positive, int32_t *negatives, int32_t *n_valid,
+                  int32_t *pos_attempts, int32_t *neg_draws, int nthreads)
+{
+    if (!g || !a || qtype < 0 || qtype > 8) return -1;
+    if (a->batch < 0 || a->n_neg < 0 || a->pos_tries < 1 || a->neg_tries < a->n_neg) return -1;
+    if (a->query_offset + (uint64_t)a->batch > (1ULL << 32)) return -1;
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+    const otype *T = &TYPES[qtype];
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+    for (int64_t b = 0; b < a->batch; b++)
+        sample_one(g, T, a, b, anchors, relations, positive, negatives, n_valid, pos_attempts,
+                   neg_draws);
+    return 0;
+}
+
+/* --------------------------------------------------- bidirectional check */
+/* Sec. 3.2, bidirectional rejection sampling: the sets at the cut nodes are
+   computed from the anchors (forward caching); the candidate is expanded
+   from the root towards the cut (backward verification) and accepted as an
+   answer iff the two sides meet. */
+typedef struct {
+    const okg *g;
+    const otype *T;
+    uint32_t cut;
+    iset F[8];
+    const int32_t *relations;
+    const int32_t *anchors;
+    int64_t visited;
+} bidir;
+
+static int member(bidir *B, int k, int32_t x)
+{
+    if (B->cut & (1u << k)) return set_has(B->F[k], x);
+    const onode *nd = &B->T->nd[k];
+    if (nd->op == N_ANCHOR) return x == B->anchors[nd->slot];
+    if (nd->op == N_PROJ) {
+        /* x is in A_r(S) iff some y with (y, r, x) in E lies in S */
+        int64_t b, e;
+        rel_range(B->g->r_off, B->g->r_rel, x, B->relations[nd->slot], &b, &e);
+        B->visited += e - b;
+        for (int64_t i = b; i < e; i++)
+            if (member(B, nd->ch[0], B->g->r_nbr[i])) return 1;
+        return 0;
+    }
+    for (int c = 0; c < nd->nch; c++) {
+        int in = member(B, nd->ch[c], x);
+        if (nd->op == N_AND && !in) return 0;
+        if (nd->op == N_OR && in) return 1;
+    }
+    return nd->op == N_AND;
+}
+
+/* Def. of a node cut: every anchor-to-root path meets the cut exactly once. */
+static int is_node_cut(const otype *T, uint32_t mask)
+{
+    if (mask >> T->n) return 0;
+    int parent[8];
+    for (int k = 0; k < T->n; k++) parent[k] = -1;
+    for (int k = 0; k < T->n; k++)
+        for (int c = 0; c < T->nd[k].nch; c++) parent[T->nd[k].ch[c]] = k;
+    for (int k = 0; k < T->n; k++) {
+        if (T->nd[k].op != N_ANCHOR) continue;
+        int hits = 0;
+        for (int v = k; v != -1; v = parent[v]) hits += (mask >> v) & 1;
+        if (hits != 1) return 0;
+    }
+    return 1;
+}
+
+int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const int32_t *relations,
+                       uint32_t cut_mask, int32_t c, int64_t *counts)
+{
+    if (qtype < 0 || qtype > 8 || c < 0 || c >= g->V) return -1;
+    const otype *T = &TYPES[qtype];
+    if (!is_node_cut(T, cut_mask)) return -1;
+    bidir B;
+    memset(&B, 0, sizeof(B));
+    B.g = g; B.T = T; B.cut = cut_mask; B.relations = relations; B.anchors = anchors;
+    int64_t fwd = 0;
+    for (int k = 0; k < T->n; k++)
+        if (cut_mask & (1u << k)) {
+            B.F[k] = eval_node(g, T, k, anchors, relations);
+            fwd += B.F[k].n;
+        }
+    int in = member(&B, T->root, c);
+    for (int k = 0; k < T->n; k++) free(B.F[k].v);
+    if (counts) { counts[0] = fwd; counts[1] = B.visited; }
+    return in;
+}
