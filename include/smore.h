@@ -1,0 +1,190 @@
+/*
+ * smore.h -- C ABI of the MI355X sampler for multi-hop query training data
+ * (SMORE, arXiv 2110.14890: reverse directional sampling of queries, Sec. 3.1,
+ * and bidirectional rejection sampling of verified negatives, Sec. 3.2).
+ *
+ * Conventions
+ *  - Every call returns SMORE_OK (0) or a negative SMORE_E_* code; on error
+ *    smore_last_error() returns a message for the calling thread.  No C++
+ *    exception crosses this boundary.
+ *  - Arguments are validated synchronously on the host before any launch;
+ *    an invalid call launches nothing and writes nothing.
+ *  - Pointers named *_host are host memory, all other buffers are device
+ *    memory allocated by the caller (for example torch tensors on the same
+ *    device).  The library never frees caller memory.
+ *  - smore_sample is asynchronous on the caller's HIP stream and returns
+ *    without synchronising; results are valid once that stream reaches them.
+ *  - All ids and outputs are int32.  Entity ids are in [0, V), relation ids
+ *    in [0, R') where R' = 2R when the graph adds inverse relations.
+ */
+#ifndef SMORE_H
+#define SMORE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    SMORE_OK = 0,
+    SMORE_E_INVALID_ARG = -1, /* null pointer, bad size, bad query plan */
+    SMORE_E_RANGE = -2,       /* an id outside [0, V) or [0, R) */
+    SMORE_E_UNSUPPORTED = -3, /* plan outside the nine shapes, negation, limits */
+    SMORE_E_NOMEM = -4,       /* device or host allocation failed */
+    SMORE_E_HIP = -5,         /* a HIP runtime call failed */
+    SMORE_E_OVERFLOW = -6     /* counts beyond the int32 / 32-bit query-id range */
+};
+
+/* flags of smore_build_graph */
+#define SMORE_ADD_INVERSE 1u /* also insert (t, r + R, h) for every (h, r, t) */
+
+/* Node operators of a query computation plan (Sec. 2, "Query computation
+   plan"; appendix on the computation plan).  Each node is a set of
+   entities; a projection node applies one relation to its single child, an
+   intersection / union node combines its children, an anchor is a leaf. */
+enum { SMORE_OP_ANCHOR = 0, SMORE_OP_PROJ = 1, SMORE_OP_AND = 2, SMORE_OP_OR = 3, SMORE_OP_NOT = 4 };
+
+/* One plan node.  child[] index earlier nodes of the same plan (children
+   before parents).  slot: the anchor slot (0..2) of an anchor, the relation
+   slot (0..2) of a projection, -1 otherwise. */
+typedef struct {
+    int32_t op, n_child, child[3], slot;
+} smore_dag_node;
+
+/* A plan tree: n_nodes nodes, root = the answer node V_?. */
+typedef struct {
+    int32_t n_nodes, root;
+    smore_dag_node node[16];
+} smore_query_dag;
+
+/* Arguments of one sampling call.
+   batch        number of queries B (>= 1)
+   n_neg        negatives wanted per query (>= 0)
+   pos_tries    reverse-sampling attempts per query (>= 1)
+   neg_tries    candidate draws per query (>= n_neg, <= SMORE_MAX_NEG_TRIES)
+   max_fanout   0, or reject a grounding whose step (x, r) -> e has
+                |A_r(x)| > max_fanout (the paper's per-relation expansion C)
+   seed         64-bit key of the counter-based draws
+   query_offset query q of this call has id query_offset + q; the result of
+                a query depends only on (graph, plan, seed, id, counts), so a
+                batch split over several calls gives identical rows
+   flags        0 (reserved) */
+typedef struct {
+    int32_t batch, n_neg, pos_tries, neg_tries, max_fanout;
+    uint64_t seed, query_offset;
+    uint32_t flags;
+} smore_sample_args;
+
+#define SMORE_MAX_NEG_TRIES 4096
+
+/* Caller-owned device outputs, int32, row-major.
+   anchors   [B,3]   anchor entities by slot, -1 for unused slots
+   relations [B,3]   relations by slot, -1 for unused slots
+   positive  [B]     the answer entity grounded at the root
+   negatives [B,n_neg] verified non-answers in draw order, -1 padded
+   n_valid   [B]     number of negatives found; -1 if no positive was found
+   pos_attempts [B]  attempts used (1-based); pos_tries when none succeeded
+   neg_draws [B]     draws consumed: 1 + index of the n_neg-th accepted
+                     draw, else neg_tries; 0 when n_neg = 0; -1 with no positive
+   All seven pointers are required. */
+typedef struct {
+    int32_t *anchors, *relations, *positive, *negatives, *n_valid, *pos_attempts, *neg_draws;
+} smore_sample_out;
+
+typedef struct smore_graph smore_graph; /* opaque; owns its device arrays */
+
+/* Build forward and reverse adjacency on the current HIP device from
+   n_triples host triples (h, r, t) (int32 [n_triples, 3]).  The KG is a set
+   of triples (Sec. 2), so duplicates are removed.  Adjacency is grouped by
+   (entity, relation) with ascending relations per entity and ascending
+   neighbours per group, as sorted lists (appendix on the optimal cut: sets
+   kept as sorted lists).  Errors: SMORE_E_RANGE for an id outside
+   [0, n_entities) / [0, n_relations); SMORE_E_OVERFLOW when the edge count
+   (doubled with SMORE_ADD_INVERSE) reaches 2^31; SMORE_E_NOMEM; SMORE_E_HIP.
+   Synchronous.  *out must be released with smore_free_graph. */
+int smore_build_graph(const int32_t *triples_host, int64_t n_triples, int32_t n_entities,
+                      int32_t n_relations, uint32_t flags, smore_graph **out);
+
+/* Sizes of a built graph (any pointer may be NULL): entities, relations
+   (after inverse), unique edges, forward and reverse (entity, relation)
+   groups, device bytes held. */
+int smore_graph_info(const smore_graph *g, int64_t *n_entities, int64_t *n_relations,
+                     int64_t *n_edges, int64_t *n_seg_fwd, int64_t *n_seg_rev,
+                     int64_t *device_bytes);
+
+/* Copy one device array of the graph to host memory (for tests and
+   inspection).  which: 0 fwd node_ptr [V+1], 1 fwd groups [2*(S_fwd+1)]
+   (relation, first edge) pairs, 2 fwd neighbours [E], 3 rev node_ptr,
+   4 rev groups, 5 rev neighbours, 6 active_in (entities with an in-edge,
+   ascending).  count must equal the array length.  Synchronous. */
+int smore_graph_copy(const smore_graph *g, int32_t which, int32_t *host_dst, int64_t count);
+
+/* Fill *out with one of the nine negation-free shapes "1p" "2p" "3p" "2i"
+   "3i" "ip" "pi" "2u" "up" (Sec. 5.1: the query structures of BetaE).
+   Anchor and relation slots follow branch order, and within a branch run
+   from the anchor to the root. */
+int smore_query_preset(const char *name, smore_query_dag *out);
+
+/* Node cut of a plan tree minimising the worst per-anchor-path cost
+   max(C^i, C^(t-i)) (Sec. 3.2, Def. "Node cut" and the optimal-scheduling
+   equation), by the dynamic program of the appendix on the optimal cut
+   (u = projections to the root, s = longest projection path to an anchor,
+   o = best cost) and its top-down construction.  tie_break 0 adds a node
+   when the children's best cost exceeds its own (as stated); 1 also adds it
+   on equality, which caches as far forward as the same cost allows.
+   cut_nodes receives up to 16 node indices; *n_cut their number. */
+int smore_plan(const smore_query_dag *dag, int32_t tie_break, int32_t *cut_nodes, int32_t *n_cut);
+
+/* Device workspace smore_sample needs for these arguments (currently 0:
+   everything lives in registers and LDS).  workspace may then be NULL. */
+int smore_sample_workspace_bytes(const smore_graph *g, const smore_query_dag *dag,
+                                 const smore_sample_args *args, size_t *bytes);
+
+/* Sample args->batch queries of shape dag with one positive each and up to
+   n_neg verified negatives (Sec. 3.1 reverse directional sampling; Sec. 3.2
+   bidirectional rejection sampling with a constant candidate budget).
+   Per query id q: attempt t grounds the root uniformly among entities with
+   an in-edge, then walks from the root to the anchors in pre-order, each
+   projection picking an in-relation uniformly and then an in-neighbour
+   uniformly; the first attempt without a dead end, a repeated
+   (anchor, relation) pair among single-projection siblings, or a step wider
+   than max_fanout wins.  Candidate j (j < neg_tries) is uniform over all V
+   entities and is kept iff it is not an answer of the query and was not
+   drawn earlier; the first n_neg kept are returned.  Draws come from
+   Philox4x32-10 with counter (j, t, q, tag) and key seed.  The plan must
+   be one of the nine presets (SMORE_E_UNSUPPORTED otherwise, including
+   negation).  hip_stream: a hipStream_t, or NULL for the default stream. */
+int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_sample_args *args,
+                 const smore_sample_out *out, void *workspace, size_t ws_bytes, void *hip_stream);
+
+/* The two stages of smore_sample, for callers that time or feed them
+   separately.  Same arguments and validation as smore_sample.
+   smore_sample_positives writes anchors, relations, positive, pos_attempts
+   and n_valid (-1 for a query without a positive, else 0).
+   smore_sample_negatives reads anchors, relations and positive (a row with
+   positive < 0, or with an anchor or relation id used by the shape outside
+   the graph's range, is skipped: negatives -1, n_valid -1, neg_draws -1) and
+   writes negatives, n_valid and neg_draws; it may be run on queries built
+   by the caller.  stats is NULL or a device int64 [batch, 2] array that
+   receives, per query, the bytes and the 64-byte lines of graph data the
+   verification had to read (the accounting used for roofline figures);
+   counting makes the call slower and does not change any other output. */
+int smore_sample_positives(const smore_graph *g, const smore_query_dag *dag,
+                           const smore_sample_args *args, const smore_sample_out *out,
+                           void *hip_stream);
+int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
+                           const smore_sample_args *args, const smore_sample_out *out,
+                           int64_t *stats, void *hip_stream);
+
+/* Release a graph (NULL is a no-op). */
+void smore_free_graph(smore_graph *g);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *smore_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SMORE_H */

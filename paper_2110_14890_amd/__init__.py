@@ -1,0 +1,218 @@
+"""MI355X-native sampler of multi-hop query training data (SMORE, arXiv 2110.14890).
+
+Thin Python binding over the C ABI of ``libsmore.so`` (declared in
+``include/smore.h``).  It only marshals arguments: graph building, reverse
+directional sampling of positives and bidirectional rejection sampling of
+negatives all run in the library's HIP kernels.  PyTorch provides device
+memory and the current HIP stream.  There is no CPU fallback: if the library
+is not built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsmore.so")
+
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+ADD_INVERSE = 1
+MAX_NEG_TRIES = 4096
+OP_ANCHOR, OP_PROJ, OP_AND, OP_OR, OP_NOT = range(5)
+ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "RANGE", -3: "UNSUPPORTED", -4: "NOMEM", -5: "HIP",
+          -6: "OVERFLOW"}
+
+c_i32, c_i64, c_u32, c_u64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
+
+
+class DagNode(ctypes.Structure):
+    _fields_ = [("op", c_i32), ("n_child", c_i32), ("child", c_i32 * 3), ("slot", c_i32)]
+
+
+class QueryDag(ctypes.Structure):
+    _fields_ = [("n_nodes", c_i32), ("root", c_i32), ("node", DagNode * 16)]
+
+
+class SampleArgs(ctypes.Structure):
+    _fields_ = [("batch", c_i32), ("n_neg", c_i32), ("pos_tries", c_i32), ("neg_tries", c_i32),
+                ("max_fanout", c_i32), ("seed", c_u64), ("query_offset", c_u64), ("flags", c_u32)]
+
+
+class SampleOut(ctypes.Structure):
+    _fields_ = [(n, c_vp) for n in ("anchors", "relations", "positive", "negatives", "n_valid",
+                                    "pos_attempts", "neg_draws")]
+
+
+OUT_FIELDS = ("anchors", "relations", "positive", "negatives", "n_valid", "pos_attempts",
+              "neg_draws")
+
+
+class SmoreError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                               "(python paper_2110_14890_amd/build.py)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.smore_last_error.restype = ctypes.c_char_p
+        L.smore_build_graph.argtypes = [c_vp, c_i64, c_i32, c_i32, c_u32, ctypes.POINTER(c_vp)]
+        L.smore_graph_info.argtypes = [c_vp] + [ctypes.POINTER(c_i64)] * 6
+        L.smore_graph_copy.argtypes = [c_vp, c_i32, c_vp, c_i64]
+        L.smore_query_preset.argtypes = [ctypes.c_char_p, ctypes.POINTER(QueryDag)]
+        L.smore_plan.argtypes = [ctypes.POINTER(QueryDag), c_i32, ctypes.POINTER(c_i32),
+                                 ctypes.POINTER(c_i32)]
+        L.smore_sample_workspace_bytes.argtypes = [c_vp, ctypes.POINTER(QueryDag),
+                                                   ctypes.POINTER(SampleArgs),
+                                                   ctypes.POINTER(ctypes.c_size_t)]
+        L.smore_sample.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
+                                   ctypes.POINTER(SampleOut), c_vp, ctypes.c_size_t, c_vp]
+        L.smore_sample_positives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
+                                             ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
+                                             c_vp]
+        L.smore_sample_negatives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
+                                             ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
+                                             c_vp, c_vp]
+        L.smore_free_graph.argtypes = [c_vp]
+        L.smore_free_graph.restype = None
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().smore_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise SmoreError(rc, last_error())
+
+
+def query_preset(name: str) -> QueryDag:
+    d = QueryDag()
+    _check(lib().smore_query_preset(name.encode(), ctypes.byref(d)))
+    return d
+
+
+def plan(dag: "QueryDag | str", tie_break: int = 0) -> list:
+    if isinstance(dag, str):
+        dag = query_preset(dag)
+    cut = (c_i32 * 16)()
+    n = c_i32()
+    _check(lib().smore_plan(ctypes.byref(dag), tie_break, cut, ctypes.byref(n)))
+    return [cut[k] for k in range(n.value)]
+
+
+class Graph:
+    """Device adjacency owned by the library (smore_build_graph / smore_free_graph)."""
+
+    def __init__(self, triples, n_entities: int, n_relations: int, add_inverse: bool = False):
+        tr = np.ascontiguousarray(triples, dtype=np.int32).reshape(-1, 3)
+        h = c_vp()
+        _check(lib().smore_build_graph(tr.ctypes.data if len(tr) else None, len(tr), n_entities,
+                                       n_relations, ADD_INVERSE if add_inverse else 0,
+                                       ctypes.byref(h)))
+        self._h = h
+        vals = [c_i64() for _ in range(6)]
+        _check(lib().smore_graph_info(h, *[ctypes.byref(v) for v in vals]))
+        (self.V, self.R, self.E, self.S_fwd, self.S_rev, self.device_bytes) = [v.value for v in vals]
+
+    @property
+    def handle(self):
+        return self._h
+
+    _SIZES = {0: "V+1", 1: "2*(S_fwd+1)", 2: "E", 3: "V+1", 4: "2*(S_rev+1)", 5: "E", 6: "A"}
+
+    def copy(self, which: int, count: int) -> np.ndarray:
+        out = np.zeros(max(count, 1), np.int32)
+        _check(lib().smore_graph_copy(self._h, which, out.ctypes.data, count))
+        return out[:count]
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            lib().smore_free_graph(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_graph(triples, n_entities: int, n_relations: int, add_inverse: bool = False) -> Graph:
+    return Graph(triples, n_entities, n_relations, add_inverse)
+
+
+def make_args(batch: int, n_neg: int, seed: int = 0, query_offset: int = 0, pos_tries: int = 64,
+              neg_tries: int | None = None, max_fanout: int = 0, flags: int = 0) -> SampleArgs:
+    if neg_tries is None:
+        neg_tries = 4 * n_neg
+    return SampleArgs(batch, n_neg, pos_tries, neg_tries, max_fanout, seed, query_offset, flags)
+
+
+def alloc_outputs(batch: int, n_neg: int, device=None) -> dict:
+    import torch
+    dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
+    z = lambda *s: torch.empty(s, dtype=torch.int32, device=dev)
+    return {"anchors": z(batch, 3), "relations": z(batch, 3), "positive": z(batch),
+            "negatives": z(batch, n_neg), "n_valid": z(batch), "pos_attempts": z(batch),
+            "neg_draws": z(batch)}
+
+
+def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None) -> dict:
+    """smore_sample into caller-owned torch tensors on the current (or given) stream."""
+    _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                              ctypes.byref(_out_struct(out)), None, 0, _stream_handle(stream)))
+    return out
+
+
+def _out_struct(out: dict) -> SampleOut:
+    return SampleOut(*[out[k].data_ptr() if k in out and out[k].numel() else None
+                       for k in OUT_FIELDS])
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return c_vp(stream.cuda_stream)
+
+
+def sample_positives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None) -> dict:
+    """First stage only (smore_sample_positives): anchors, relations, positive,
+    pos_attempts, n_valid."""
+    _check(lib().smore_sample_positives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                        ctypes.byref(_out_struct(out)), _stream_handle(stream)))
+    return out
+
+
+def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stats=None,
+                     stream=None) -> dict:
+    """Second stage only (smore_sample_negatives) on the queries in `out`;
+    stats: optional int64 [batch, 2] device tensor of (bytes, 64-byte lines)
+    of graph data read per query."""
+    sp = c_vp(stats.data_ptr()) if stats is not None else None
+    _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                        ctypes.byref(_out_struct(out)), sp, _stream_handle(stream)))
+    return out
+
+
+def sample(graph: Graph, qtype: "str | QueryDag", batch: int, n_neg: int, seed: int = 0,
+           query_offset: int = 0, pos_tries: int = 64, neg_tries: int | None = None,
+           max_fanout: int = 0, stream=None) -> dict:
+    """Sample `batch` queries: dict of int32 device tensors (see include/smore.h)."""
+    dag = query_preset(qtype) if isinstance(qtype, str) else qtype
+    args = make_args(batch, n_neg, seed, query_offset, pos_tries, neg_tries, max_fanout)
+    out = alloc_outputs(batch, n_neg)
+    return sample_into(graph, dag, args, out, stream)

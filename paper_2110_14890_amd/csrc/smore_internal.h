@@ -1,0 +1,75 @@
+// smore_internal.h -- types shared by the host C ABI and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/smore.h"
+
+namespace smore {
+
+// Device-resident adjacency of one direction (forward: entity -> tails by
+// relation; reverse: entity -> heads by relation).
+//   node[v] .. node[v+1]   : groups (one per relation) of entity v, v in [0, V]
+//   grp[g] = (relation, first edge); grp[S] = (INT32_MAX, E) is a sentinel so
+//            that group g spans edges [grp[g].y, grp[g+1].y)
+//   nbr[e]                 : neighbour entity of edge e, ascending in a group
+struct DirView {
+    const int32_t* node;
+    const int2* grp;
+    const int32_t* nbr;
+};
+
+struct GraphView {
+    DirView fwd, rev;
+    const int32_t* active_in;  // entities with an in-edge, ascending
+    int32_t V;
+    int32_t n_active;
+};
+
+// Positive-sampling program compiled from a plan on the host: a pre-order
+// list of projection steps.  Register 0 holds the root; step k reads
+// register src[k], grounds relation slot rel_slot[k] and writes register
+// k + 1.  Anchor slot a takes register anchor_reg[a].  Pairs of single-
+// projection siblings under an intersection or union must differ in
+// (anchor, relation).
+struct WalkProgram {
+    int32_t n_steps;
+    int32_t src[3];
+    int32_t rel_slot[3];
+    int32_t n_anchor;
+    int32_t anchor_reg[3];
+    int32_t n_pairs;
+    int32_t pair_anchor[3][2];
+    int32_t pair_rel[3][2];
+};
+
+// Query shapes with a dedicated verification kernel.
+enum QType { Q1P = 0, Q2P, Q3P, Q2I, Q3I, QIP, QPI, Q2U, QUP, NQTYPE };
+
+struct SampleParams {
+    int32_t batch, n_neg, pos_tries, neg_tries, max_fanout;
+    uint64_t seed, query_offset;
+};
+
+}  // namespace smore
+
+struct smore_graph {
+    int device;
+    int32_t V, R;
+    int64_t E, S_fwd, S_rev, n_active;
+    int32_t *f_node, *f_nbr, *r_node, *r_nbr, *active_in;
+    int2 *f_grp, *r_grp;
+    size_t bytes;
+};
+
+// Entry points implemented in the .hip files (host side, C++ linkage).
+namespace smore {
+int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_t R,
+                       bool add_inverse, smore_graph* g, const char** err);
+int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
+                    const smore_sample_out& out, hipStream_t stream, const char** err);
+int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
+                    const smore_sample_out& out, int64_t* stats, hipStream_t stream,
+                    const char** err);
+}  // namespace smore

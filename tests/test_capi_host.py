@@ -1,0 +1,213 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+- the library loads and exports every function include/smore.h declares;
+- the nine presets encode the same plans as the oracle's (Sec. 2 plans);
+- the planner (appendix on the optimal cut: DP over u, s, o plus top-down
+  construction) returns a node cut (Def. "Node cut") whose cost equals the
+  brute-force minimum of the optimal-scheduling objective, for the presets
+  and for random plan trees, with both tie-break rules;
+- the tie_break 0 cuts of the presets;
+- argument validation of smore_sample / smore_plan / smore_build_graph
+  happens on the host before any device call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2110_14890_amd as sm
+from oracle import cuts as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "smore.h")
+TYPES = sm.TYPES
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(sm.LIB_PATH):
+        from paper_2110_14890_amd import build
+        build.build()
+    return sm.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|int|void)\s*(smore_\w+)\s*\(", text,
+                                 re.M)))
+
+
+def test_exports_every_declared_function(L):
+    names = declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def dag_arrays(d):
+    n = d.n_nodes
+    op = [d.node[k].op for k in range(n)]
+    ch = [[d.node[k].child[c] if c < d.node[k].n_child else -1 for c in range(3)] for k in range(n)]
+    sl = [d.node[k].slot if d.node[k].op in (0, 1) else -1 for k in range(n)]
+    return op, ch, sl, d.root
+
+
+@pytest.mark.parametrize("qtype", TYPES)
+def test_presets_match_oracle_plans(L, oracle_lib, qtype):
+    op, ch, sl, root = dag_arrays(sm.query_preset(qtype))
+    oop, och, osl, oroot = oracle_lib.type_plan(qtype)
+    assert op == list(oop) and ch == och.tolist() and sl == list(osl) and root == oroot
+
+
+STRICT_CUTS = {"1p": [0], "2p": [1], "3p": [1], "2i": [0, 2], "3i": [0, 2, 4], "ip": [1, 3],
+               "pi": [1, 3], "2u": [0, 2], "up": [1, 3]}
+FORWARD_CUTS = {"1p": [1], "2p": [1], "3p": [2], "2i": [4], "3i": [6], "ip": [4], "pi": [1, 4],
+                "2u": [4], "up": [4]}
+
+
+@pytest.mark.parametrize("qtype", TYPES)
+def test_preset_cuts(L, qtype):
+    assert sorted(sm.plan(qtype, 0)) == STRICT_CUTS[qtype]
+    assert sorted(sm.plan(qtype, 1)) == FORWARD_CUTS[qtype]
+
+
+@pytest.mark.parametrize("qtype", TYPES)
+@pytest.mark.parametrize("tie", [0, 1])
+def test_preset_cut_is_optimal(L, qtype, tie):
+    op, ch, sl, root = dag_arrays(sm.query_preset(qtype))
+    cut = set(sm.plan(qtype, tie))
+    assert C.is_cut(op, ch, root, cut)
+    best, _ = C.optimal(op, ch, root)
+    assert C.cost(op, ch, root, cut) == best
+
+
+def random_tree(rng, max_nodes=12):
+    """Random plan tree, children before parents (anchors, projections,
+    negations, and/or with 2-3 children)."""
+    nodes = []          # (op, children, slot)
+    forest = []
+    n_anchor = int(rng.integers(1, 4))
+    for a in range(n_anchor):
+        nodes.append((0, [], a))
+        forest.append(len(nodes) - 1)
+    rel_slot = 0
+    while len(nodes) < max_nodes and (len(forest) > 1 or rng.random() < 0.6):
+        if len(forest) >= 2 and rng.random() < 0.4:
+            k = int(min(len(forest), rng.integers(2, 4)))
+            idx = sorted(rng.choice(len(forest), k, replace=False).tolist(), reverse=True)
+            kids = [forest.pop(i) for i in idx]
+            nodes.append((int(rng.choice([2, 3])), sorted(kids), -1))
+        else:
+            i = int(rng.integers(0, len(forest)))
+            op = 4 if (rng.random() < 0.15 and nodes[forest[i]][0] != 4) else 1
+            nodes.append((op, [forest[i]], rel_slot % 3 if op == 1 else -1))
+            if op == 1:
+                rel_slot += 1
+        if nodes[-1][0] in (2, 3):
+            forest.append(len(nodes) - 1)
+        else:
+            forest[i] = len(nodes) - 1
+    while len(forest) > 1:
+        kids = sorted(forest[:3])
+        forest = forest[3:]
+        nodes.append((2, kids, -1))
+        forest.append(len(nodes) - 1)
+    if len(nodes) > 16:
+        return None
+    d = sm.QueryDag()
+    d.n_nodes = len(nodes)
+    d.root = len(nodes) - 1
+    for k, (op, kids, slot) in enumerate(nodes):
+        d.node[k].op = op
+        d.node[k].n_child = len(kids)
+        for c in range(3):
+            d.node[k].child[c] = kids[c] if c < len(kids) else -1
+        d.node[k].slot = slot
+    return d
+
+
+def test_random_trees_cut_is_optimal(L):
+    rng = np.random.default_rng(1)
+    checked = 0
+    for _ in range(400):
+        d = random_tree(rng)
+        if d is None:
+            continue
+        op, ch, sl, root = dag_arrays(d)
+        best, _ = C.optimal(op, ch, root)
+        for tie in (0, 1):
+            cut = set(sm.plan(d, tie))
+            assert C.is_cut(op, ch, root, cut), (op, ch, cut)
+            assert C.cost(op, ch, root, cut) == best, (op, ch, cut)
+        checked += 1
+    assert checked > 200
+
+
+def _expect(rc, code):
+    assert rc == code, (rc, sm.last_error())
+
+
+def test_plan_rejects_bad_trees(L):
+    d = sm.query_preset("2p")
+    n = (ctypes.c_int32 * 16)()
+    k = ctypes.c_int32()
+    bad = sm.QueryDag.from_buffer_copy(d)
+    bad.node[1].child[0] = 2                      # child after parent
+    _expect(L.smore_plan(ctypes.byref(bad), 0, n, ctypes.byref(k)), -1)
+    bad = sm.QueryDag.from_buffer_copy(d)
+    bad.node[1].slot = 3                          # slot outside 0..2
+    _expect(L.smore_plan(ctypes.byref(bad), 0, n, ctypes.byref(k)), -1)
+    bad = sm.QueryDag.from_buffer_copy(d)
+    bad.node[2].n_child = 2                       # projection with two children
+    _expect(L.smore_plan(ctypes.byref(bad), 0, n, ctypes.byref(k)), -1)
+    bad = sm.QueryDag.from_buffer_copy(d)
+    bad.root = 1                                  # node 2 left without a parent
+    _expect(L.smore_plan(ctypes.byref(bad), 0, n, ctypes.byref(k)), -1)
+    _expect(L.smore_plan(ctypes.byref(d), 2, n, ctypes.byref(k)), -1)
+    dd = sm.QueryDag()
+    _expect(L.smore_query_preset(b"4p", ctypes.byref(dd)), -3)
+
+
+def _call_sample(L, dag, args, out_ptrs):
+    so = sm.SampleOut(*out_ptrs)
+    return L.smore_sample(None, ctypes.byref(dag), ctypes.byref(args), ctypes.byref(so), None, 0, None)
+
+
+def test_sample_validation_on_host(L):
+    buf = (ctypes.c_int32 * 64)()
+    ptrs = [ctypes.addressof(buf)] * 7
+    dag = sm.query_preset("2p")
+    good = sm.make_args(4, 2)
+    _expect(_call_sample(L, dag, good, ptrs), -1)                 # graph is NULL (checked last)
+    assert "graph" in sm.last_error()
+    for field, val, code in [("batch", 0, -1), ("n_neg", -1, -1), ("pos_tries", 0, -1),
+                             ("neg_tries", 1, -1), ("neg_tries", sm.MAX_NEG_TRIES + 1, -3),
+                             ("max_fanout", -1, -1), ("flags", 1, -1),
+                             ("query_offset", 2**32 - 3, -6)]:
+        a = sm.make_args(4, 2)
+        setattr(a, field, val)
+        _expect(_call_sample(L, dag, a, ptrs), code)
+    _expect(_call_sample(L, dag, good, ptrs[:3] + [None] + ptrs[4:]), -1)   # negatives NULL
+    a0 = sm.make_args(4, 0)
+    _call_sample(L, dag, a0, ptrs[:3] + [None] + ptrs[4:])
+    assert "graph" in sm.last_error()                                          # n_neg 0: allowed
+    neg = sm.QueryDag.from_buffer_copy(dag)
+    neg.node[2].op = sm.OP_NOT
+    neg.node[2].slot = -1
+    _expect(_call_sample(L, neg, good, ptrs), -3)                 # negation
+    other = sm.QueryDag.from_buffer_copy(sm.query_preset("2i"))
+    other.node[4].child[0], other.node[4].child[1] = 3, 1         # same tree, other order
+    _expect(_call_sample(L, other, good, ptrs), -3)
+
+
+def test_build_graph_validation_on_host(L):
+    g = ctypes.c_void_p()
+    tr = (ctypes.c_int32 * 3)(0, 0, 1)
+    _expect(L.smore_build_graph(tr, 1, 0, 1, 0, ctypes.byref(g)), -1)
+    _expect(L.smore_build_graph(tr, 1, 2, 1, 8, ctypes.byref(g)), -1)
+    _expect(L.smore_build_graph(None, 1, 2, 1, 0, ctypes.byref(g)), -1)
+    _expect(L.smore_build_graph(tr, 2**31, 2, 1, 0, ctypes.byref(g)), -6)
+    _expect(L.smore_build_graph(tr, 2**30, 2, 1, sm.ADD_INVERSE, ctypes.byref(g)), -6)
+    assert not g.value

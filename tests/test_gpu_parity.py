@@ -1,0 +1,178 @@
+"""GPU parity: the HIP path against the CPU oracle, element by element.
+
+Integer work throughout, so the bar is bit-exact equality of every output
+array (anchors, relations, positive, negatives, n_valid, pos_attempts,
+neg_draws) and of the device adjacency.  Inputs are the seeded synthetic
+KGs of kgsynth (stand-ins for the paper's datasets) and small hand-made
+graphs for the degenerate cases.
+"""
+import numpy as np
+import pytest
+
+import kgsynth
+import paper_2110_14890_amd as sm
+from gpu_common import (assert_same, config_graph, gpu_sample, graph_pair, oracle_rows, progress,
+                        require_gpu, to_numpy)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def expand(node, grp, nbr, V):
+    grp = grp.reshape(-1, 2)
+    assert grp[0, 1] == 0 and grp[-1, 0] == np.iinfo(np.int32).max and grp[-1, 1] == len(nbr)
+    seg_len = np.diff(grp[:, 1])
+    assert (seg_len > 0).all()
+    ent_of_grp = np.repeat(np.arange(V, dtype=np.int32), np.diff(node))
+    return (np.repeat(ent_of_grp, seg_len), np.repeat(grp[:-1, 0], seg_len), nbr)
+
+
+def check_graph(g, og):
+    assert (g.V, g.R, g.E, g.S_fwd, g.S_rev) == (og.V, og.R, og.E, og.S_fwd, og.S_rev)
+    for d, (n_i, g_i, e_i, S) in enumerate([(0, 1, 2, g.S_fwd), (3, 4, 5, g.S_rev)]):
+        node = g.copy(n_i, g.V + 1)
+        grp = g.copy(g_i, 2 * (S + 1))
+        nbr = g.copy(e_i, g.E)
+        ent, rel, nb = expand(node, grp, nbr, g.V)
+        oe, orl, onb = og.dump(reverse=bool(d))
+        assert np.array_equal(ent, oe) and np.array_equal(rel, orl) and np.array_equal(nb, onb), d
+    assert np.array_equal(g.copy(6, og.n_active), og.active_in())
+
+
+@pytest.mark.parametrize("case", ["dups", "dups_inverse", "tiny", "fb15k237", "fb400k", "empty",
+                                  "one_entity"])
+def test_graph_build_matches_oracle(case):
+    rng = np.random.default_rng(5)
+    if case in ("dups", "dups_inverse"):
+        tr, V, R, inv = kgsynth.random_tiny(rng, 50, 4, 2000), 50, 4, case == "dups_inverse"
+    elif case == "empty":
+        tr, V, R, inv = np.zeros((0, 3), np.int32), 10, 2, False
+    elif case == "one_entity":
+        tr, V, R, inv = np.array([[0, 0, 0], [0, 0, 0], [0, 1, 0]], np.int32), 1, 2, True
+    else:
+        cfg, tr = config_graph(case)
+        V, R, inv = cfg.n_entities, cfg.n_relations, cfg.add_inverse
+    g, og = graph_pair(tr, V, R, inv)
+    check_graph(g, og)
+
+
+def test_graph_build_rejects_bad_ids():
+    for bad in ([[0, 0, 5]], [[0, 3, 1]], [[-1, 0, 1]]):
+        with pytest.raises(sm.SmoreError) as e:
+            sm.Graph(np.array(bad, np.int32), 5, 3)
+        assert e.value.code == -2
+
+
+FULL = [("tiny", None), ("fb15k237", None), ("fb400k", None)]
+
+
+@pytest.mark.parametrize("name", ["tiny", "fb15k237", "fb400k"])
+def test_sample_parity_full_batch(name):
+    cfg, tr = config_graph(name)
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
+    for qt in cfg.query_types:
+        progress(f"{name} {qt} batch {cfg.batch} n_neg {cfg.n_neg}")
+        got = gpu_sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        ref = og.sample(qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        assert_same(got, ref, what=f"{name}/{qt}")
+        assert (got["n_valid"] >= 0).mean() > 0.5
+
+
+@pytest.mark.parametrize("qt", sm.TYPES)
+def test_sample_parity_all_shapes_ragged(qt):
+    # batch not a multiple of any tile, n_neg above one candidate round,
+    # several seeds and offsets, dense graph so that answers get rejected
+    rng = np.random.default_rng(11)
+    tr = kgsynth.random_tiny(rng, 3000, 6, 60000)
+    g, og = graph_pair(tr, 3000, 6, True)
+    for seed, off, n_neg, nt in [(0, 0, 37, 150), (2**64 - 1, 12345, 600, 1300),
+                                 (7, 2**32 - 300, 5, 5)]:
+        got = gpu_sample(g, qt, 300, n_neg, seed=seed, query_offset=off, neg_tries=nt)
+        ref = og.sample(qt, 300, n_neg, seed=seed, query_offset=off, neg_tries=nt)
+        assert_same(got, ref, what=f"{qt} seed {seed}")
+
+
+@pytest.mark.parametrize("qt", sm.TYPES)
+def test_budget_exhaustion_and_small_graphs(qt):
+    # few entities: many candidates are answers or repeats, the budget runs out
+    rng = np.random.default_rng(3)
+    tr = kgsynth.random_tiny(rng, 40, 2, 500)
+    g, og = graph_pair(tr, 40, 2, False)
+    for n_neg, nt, pt in [(30, 30, 1), (30, 90, 3), (0, 0, 64), (1, 1, 64), (12, 4096, 64)]:
+        got = gpu_sample(g, qt, 97, n_neg, seed=3, neg_tries=nt, pos_tries=pt)
+        ref = og.sample(qt, 97, n_neg, seed=3, neg_tries=nt, pos_tries=pt)
+        assert_same(got, ref, what=f"{qt} n_neg {n_neg} neg_tries {nt} pos_tries {pt}")
+
+
+@pytest.mark.parametrize("qt", ["1p", "2p", "3p", "ip", "pi", "up"])
+def test_max_fanout(qt):
+    cfg, tr = config_graph("fb15k237")
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations)
+    for mf in (3, 40):
+        got = gpu_sample(g, qt, 256, 16, seed=1, max_fanout=mf)
+        ref = og.sample(qt, 256, 16, seed=1, max_fanout=mf)
+        assert_same(got, ref, what=f"{qt} max_fanout {mf}")
+
+
+def test_graph_without_in_edges_of_depth():
+    # no entity can be reached twice: every 2p/3p walk dies, 1p succeeds
+    tr = np.array([[0, 0, 1], [2, 0, 3], [4, 1, 5]], np.int32)
+    g, og = graph_pair(tr, 6, 2)
+    for qt in ("1p", "2p", "3p", "2i", "ip"):
+        got = gpu_sample(g, qt, 9, 2, pos_tries=5, neg_tries=6)
+        ref = og.sample(qt, 9, 2, pos_tries=5, neg_tries=6)
+        assert_same(got, ref, what=qt)
+    g, og = graph_pair(np.zeros((0, 3), np.int32), 6, 2)
+    got = gpu_sample(g, "2p", 4, 2)
+    ref = og.sample("2p", 4, 2)
+    assert_same(got, ref, what="empty graph")
+    assert (got["n_valid"] == -1).all()
+
+
+def test_split_batch_and_repeat_are_identical():
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    for qt in ("3p", "ip", "2u"):
+        full = gpu_sample(g, qt, 512, 64, seed=9)
+        again = gpu_sample(g, qt, 512, 64, seed=9)
+        a = gpu_sample(g, qt, 200, 64, seed=9)
+        b = gpu_sample(g, qt, 312, 64, seed=9, query_offset=200)
+        for k in full:
+            assert np.array_equal(full[k], again[k])
+            assert np.array_equal(full[k], np.concatenate([a[k], b[k]]))
+        # on a side stream
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            out = sm.sample(g, qt, 512, 64, seed=9, stream=s)
+        s.synchronize()
+        for k in full:
+            assert np.array_equal(full[k], out[k].cpu().numpy())
+
+
+def test_negation_plan_is_refused_on_device_graph():
+    g = sm.Graph(np.array([[0, 0, 1]], np.int32), 2, 1)
+    d = sm.query_preset("2p")
+    d.node[2].op = sm.OP_NOT
+    with pytest.raises(sm.SmoreError) as e:
+        sm.sample(g, d, 2, 1)
+    assert e.value.code == -3
+
+
+@pytest.mark.parametrize("name", ["wikikg2"])
+def test_sample_parity_large_sampled_rows(name):
+    # full batch on the GPU in the benchmark's launch configuration; the
+    # oracle recomputes a random subset of rows one query at a time
+    cfg, tr = config_graph(name)
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
+    rng = np.random.default_rng(0)
+    for qt in cfg.query_types:
+        progress(f"{name} {qt}")
+        got = gpu_sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        rows = np.sort(rng.choice(cfg.batch, 96, replace=False))
+        ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
+        assert_same(got, ref, rows=rows, what=f"{name}/{qt}")
