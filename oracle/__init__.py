@@ -65,6 +65,8 @@ def lib():
         L.oracle_graph_stats.argtypes = [P, P]
         L.oracle_graph_edges.restype = ctypes.c_int64
         L.oracle_graph_edges.argtypes = [P, ctypes.c_int, ctypes.c_int32, P, P]
+        L.oracle_graph_dump.restype = ctypes.c_int64
+        L.oracle_graph_dump.argtypes = [P, ctypes.c_int, P, P, P]
         L.oracle_graph_active_in.restype = ctypes.c_int64
         L.oracle_graph_active_in.argtypes = [P, P]
         L.oracle_sample.argtypes = [P, ctypes.c_int, ctypes.POINTER(_Args), P, P, P, P, P, P, P,
@@ -136,6 +138,13 @@ class Graph:
         nbr = np.zeros(max(n, 1), np.int32)
         lib().oracle_graph_edges(self._h, int(reverse), v, rel.ctypes.data, nbr.ctypes.data)
         return rel[:n], nbr[:n]
+
+    def dump(self, reverse: bool = False):
+        """(entity, relation, neighbour) of every edge in canonical order."""
+        n = max(self.E, 1)
+        e, r, o = np.zeros(n, np.int32), np.zeros(n, np.int32), np.zeros(n, np.int32)
+        lib().oracle_graph_dump(self._h, int(reverse), e.ctypes.data, r.ctypes.data, o.ctypes.data)
+        return e[:self.E], r[:self.E], o[:self.E]
 
     def active_in(self):
         out = np.zeros(max(self.n_active, 1), np.int32)

@@ -264,6 +264,19 @@ int64_t oracle_graph_edges(const okg *g, int dir, int32_t v, int32_t *rel, int32
     return e - b;
 }
 
+int64_t oracle_graph_dump(const okg *g, int dir, int32_t *ent, int32_t *rel, int32_t *nbr)
+{
+    const int64_t *off = dir ? g->r_off : g->f_off;
+    const int32_t *r = dir ? g->r_rel : g->f_rel, *o = dir ? g->r_nbr : g->f_nbr;
+    for (int32_t v = 0; v < g->V; v++)
+        for (int64_t k = off[v]; k < off[v + 1]; k++) {
+            ent[k] = v;
+            rel[k] = r[k];
+            nbr[k] = o[k];
+        }
+    return g->E;
+}
+
 int64_t oracle_graph_active_in(const okg *g, int32_t *out)
 {
     if (out) memcpy(out, g->active_in, (size_t)g->n_active * 4);

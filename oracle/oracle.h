@@ -50,6 +50,9 @@ void oracle_graph_stats(const okg *g, int64_t *stats);
    rel[k], nbr[k] for its edges in canonical order; returns the count
    (call with NULL buffers to get the count). */
 int64_t oracle_graph_edges(const okg *g, int dir, int32_t v, int32_t *rel, int32_t *nbr);
+/* All edges of one direction in canonical order: ent[k] (head for dir 0,
+   tail for dir 1), rel[k], nbr[k]; arrays of length E.  Returns E. */
+int64_t oracle_graph_dump(const okg *g, int dir, int32_t *ent, int32_t *rel, int32_t *nbr);
 /* Copy active_in (entities with at least one in-edge, ascending). */
 int64_t oracle_graph_active_in(const okg *g, int32_t *out);
 
