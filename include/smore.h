@@ -137,8 +137,12 @@ int smore_query_preset(const char *name, smore_query_dag *out);
    cut_nodes receives up to 16 node indices; *n_cut their number. */
 int smore_plan(const smore_query_dag *dag, int32_t tie_break, int32_t *cut_nodes, int32_t *n_cut);
 
-/* Device workspace smore_sample needs for these arguments (currently 0:
-   everything lives in registers and LDS).  workspace may then be NULL. */
+/* Bytes of device workspace smore_sample / smore_sample_negatives need for
+   these arguments (it grows with batch * neg_tries: per-draw candidate ids
+   and states, the queue of long intersections, the lists of queries still
+   short of n_neg).  The caller allocates it; its contents need no
+   initialisation and are scratch after the call.  Calls that may overlap on
+   the device must not share a workspace. */
 int smore_sample_workspace_bytes(const smore_graph *g, const smore_query_dag *dag,
                                  const smore_sample_args *args, size_t *bytes);
 
@@ -169,14 +173,17 @@ int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_s
    writes negatives, n_valid and neg_draws; it may be run on queries built
    by the caller.  stats is NULL or a device int64 [batch, 2] array that
    receives, per query, the bytes and the 64-byte lines of graph data the
-   verification had to read (the accounting used for roofline figures);
-   counting makes the call slower and does not change any other output. */
+   verification read (forward-cached lists once per query, every read made
+   from a candidate's side; lookups inside forward-cached lists are cache
+   hits of the method and are not counted); counting makes the call slower
+   and does not change any other output.  workspace / ws_bytes as for
+   smore_sample (smore_sample_positives needs none). */
 int smore_sample_positives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
                            void *hip_stream);
 int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
-                           int64_t *stats, void *hip_stream);
+                           int64_t *stats, void *workspace, size_t ws_bytes, void *hip_stream);
 
 /* Release a graph (NULL is a no-op). */
 void smore_free_graph(smore_graph *g);

@@ -82,7 +82,7 @@ def lib() -> ctypes.CDLL:
                                              c_vp]
         L.smore_sample_negatives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
-                                             c_vp, c_vp]
+                                             c_vp, c_vp, ctypes.c_size_t, c_vp]
         L.smore_free_graph.argtypes = [c_vp]
         L.smore_free_graph.restype = None
         _lib = L
@@ -170,10 +170,48 @@ def alloc_outputs(batch: int, n_neg: int, device=None) -> dict:
             "neg_draws": z(batch)}
 
 
-def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None) -> dict:
+def workspace_bytes(dag: QueryDag, args: SampleArgs) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().smore_sample_workspace_bytes(None, ctypes.byref(dag), ctypes.byref(args),
+                                              ctypes.byref(n)))
+    return n.value
+
+
+class Workspace:
+    """Device scratch for the sampling calls, grown on demand (a uint8 torch
+    tensor).  One per stream: calls that overlap must not share it."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int):
+        import torch
+        if self.buf is None or self.buf.numel() < nbytes:
+            dev = self.device if self.device is not None else torch.device(
+                "cuda", torch.cuda.current_device())
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        return self.buf
+
+
+_default_ws = {}
+
+
+def _workspace(ws, dag, args):
+    import torch
+    if ws is None:
+        key = (torch.cuda.current_device(), torch.cuda.current_stream().cuda_stream)
+        ws = _default_ws.setdefault(key, Workspace())
+    buf = ws.get(workspace_bytes(dag, args))
+    return c_vp(buf.data_ptr()), buf.numel()
+
+
+def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
+                workspace: "Workspace | None" = None) -> dict:
     """smore_sample into caller-owned torch tensors on the current (or given) stream."""
+    wp, wn = _workspace(workspace, dag, args)
     _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
-                              ctypes.byref(_out_struct(out)), None, 0, _stream_handle(stream)))
+                              ctypes.byref(_out_struct(out)), wp, wn, _stream_handle(stream)))
     return out
 
 
@@ -198,13 +236,15 @@ def sample_positives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, s
 
 
 def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stats=None,
-                     stream=None) -> dict:
+                     stream=None, workspace: "Workspace | None" = None) -> dict:
     """Second stage only (smore_sample_negatives) on the queries in `out`;
     stats: optional int64 [batch, 2] device tensor of (bytes, 64-byte lines)
     of graph data read per query."""
     sp = c_vp(stats.data_ptr()) if stats is not None else None
+    wp, wn = _workspace(workspace, dag, args)
     _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
-                                        ctypes.byref(_out_struct(out)), sp, _stream_handle(stream)))
+                                        ctypes.byref(_out_struct(out)), sp, wp, wn,
+                                        _stream_handle(stream)))
     return out
 
 

@@ -345,8 +345,16 @@ void smore_free_graph(smore_graph* g)
 int smore_sample_workspace_bytes(const smore_graph* g, const smore_query_dag* dag,
                                  const smore_sample_args* args, size_t* bytes)
 {
-    if (!g || !dag || !args || !bytes) return fail(SMORE_E_INVALID_ARG, "NULL argument");
-    *bytes = 0;
+    (void)g;
+    if (!dag || !args || !bytes) return fail(SMORE_E_INVALID_ARG, "NULL argument");
+    if (args->batch < 1 || args->n_neg < 0 || args->neg_tries < args->n_neg ||
+        args->neg_tries > SMORE_MAX_NEG_TRIES)
+        return fail(SMORE_E_INVALID_ARG, "batch, n_neg or neg_tries out of range");
+    smore::SampleParams p{};
+    p.batch = args->batch;
+    p.n_neg = args->n_neg;
+    p.neg_tries = args->neg_tries;
+    *bytes = smore::negatives_workspace_bytes(p);
     return ok();
 }
 
@@ -358,7 +366,8 @@ enum Stage { POS = 1, NEG = 2 };
 
 // Validation shared by the sampling entry points, then the launch(es).
 int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
-               const smore_sample_out* out, int64_t* stats, void* hip_stream, int stages)
+               const smore_sample_out* out, int64_t* stats, void* workspace, size_t ws_bytes,
+               void* hip_stream, int stages)
 {
     // host-side checks first (they need no device), the graph last
     if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
@@ -419,7 +428,11 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
         if (rc) return fail(rc, "positive sampling: %s", err);
     }
     if (stages & NEG) {
-        rc = smore::launch_negative(g, (smore::QType)qt, p, *out, stats, (hipStream_t)hip_stream, &err);
+        if (a->n_neg > 0 && (!workspace || ws_bytes < smore::negatives_workspace_bytes(p)))
+            return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
+                        smore::negatives_workspace_bytes(p));
+        rc = smore::launch_negative(g, (smore::QType)qt, p, *out, stats, workspace, ws_bytes,
+                                    (hipStream_t)hip_stream, &err);
         if (rc) return fail(rc, "negative sampling: %s", err);
     }
     return ok();
@@ -432,22 +445,20 @@ extern "C" {
 int smore_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
                  const smore_sample_out* out, void* workspace, size_t ws_bytes, void* hip_stream)
 {
-    (void)workspace;
-    (void)ws_bytes;
-    return run_sample(g, dag, a, out, nullptr, hip_stream, POS | NEG);
+    return run_sample(g, dag, a, out, nullptr, workspace, ws_bytes, hip_stream, POS | NEG);
 }
 
 int smore_sample_positives(const smore_graph* g, const smore_query_dag* dag,
                            const smore_sample_args* a, const smore_sample_out* out, void* hip_stream)
 {
-    return run_sample(g, dag, a, out, nullptr, hip_stream, POS);
+    return run_sample(g, dag, a, out, nullptr, nullptr, 0, hip_stream, POS);
 }
 
 int smore_sample_negatives(const smore_graph* g, const smore_query_dag* dag,
                            const smore_sample_args* a, const smore_sample_out* out, int64_t* stats,
-                           void* hip_stream)
+                           void* workspace, size_t ws_bytes, void* hip_stream)
 {
-    return run_sample(g, dag, a, out, stats, hip_stream, NEG);
+    return run_sample(g, dag, a, out, stats, workspace, ws_bytes, hip_stream, NEG);
 }
 
 }  // extern "C"

@@ -112,11 +112,19 @@ __device__ __forceinline__ bool has(const int32_t* p, int32_t n, int32_t x, bool
     return lo < n && p[lo] == x;
 }
 
+// Membership in a forward-cached list.  The list itself is accounted once
+// per query when it is cached; lookups in it are not graph traffic of the
+// method, wherever the list lives.
 template <class T>
-__device__ __forceinline__ bool has(const FSet& s, int32_t x, T& tl)
+__device__ __forceinline__ bool has(const FSet& s, int32_t x, T&)
 {
-    return has(s.p, s.n, x, !s.lds, tl);
+    NoTally none;
+    return has(s.p, s.n, x, false, none);
 }
+
+// Wave-uniform copy of a value every lane holds (the compiler then keeps
+// loops and exits that depend on it converged).
+__device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ uint64_t lanes_below(int lane)
 {
@@ -150,7 +158,6 @@ __device__ bool wave_meet3(const int32_t* S, int32_t ns, FSet A, FSet B, int lan
     // read the shortest of the three lists, search the other two
     if (A.n < ns && A.n <= B.n) {
         for (int32_t k = 0; k < A.n; k += 64) {
-            if (!A.lds && lane == 0) tl.read(A.p + k, 4 * min(64, A.n - k));
             const bool hit = k + lane < A.n && has(B, A.p[k + lane], tl) &&
                              has(S, ns, A.p[k + lane], true, tl);
             if (__ballot(hit)) return true;
@@ -159,7 +166,6 @@ __device__ bool wave_meet3(const int32_t* S, int32_t ns, FSet A, FSet B, int lan
     }
     if (B.n < ns) {
         for (int32_t k = 0; k < B.n; k += 64) {
-            if (!B.lds && lane == 0) tl.read(B.p + k, 4 * min(64, B.n - k));
             const bool hit = k + lane < B.n && has(A, B.p[k + lane], tl) &&
                              has(S, ns, B.p[k + lane], true, tl);
             if (__ballot(hit)) return true;
@@ -250,39 +256,184 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
     out.pos_attempts[b] = t;      // t was advanced past the accepted attempt
 }
 
-// --------------------------------------------------------------- verify
-// Forward-cached lists per shape (anchor slot, relation slot) at the cut the
-// planner picks:  1p {a0}, 2p/3p {V1}, 2i/3i/2u {anchors}, ip/up {Y0, Y1},
-// pi {V1, a1}.  A cut at an anchor is tested from the anchor side (c in
-// A_r(a)), which decides the same edge.  n_anc / n_rel: slots the shape uses.
-template <int QT> struct Shape;
-template <> struct Shape<Q1P> { static constexpr int nf = 1, n_anc = 1, n_rel = 1; static constexpr int fa[3] = {0, 0, 0}, fr[3] = {0, 0, 0}; };
-template <> struct Shape<Q2P> { static constexpr int nf = 1, n_anc = 1, n_rel = 2; static constexpr int fa[3] = {0, 0, 0}, fr[3] = {0, 0, 0}; };
-template <> struct Shape<Q3P> { static constexpr int nf = 1, n_anc = 1, n_rel = 3; static constexpr int fa[3] = {0, 0, 0}, fr[3] = {0, 0, 0}; };
-template <> struct Shape<Q2I> { static constexpr int nf = 2, n_anc = 2, n_rel = 2; static constexpr int fa[3] = {0, 1, 0}, fr[3] = {0, 1, 0}; };
-template <> struct Shape<Q3I> { static constexpr int nf = 3, n_anc = 3, n_rel = 3; static constexpr int fa[3] = {0, 1, 2}, fr[3] = {0, 1, 2}; };
-template <> struct Shape<QIP> { static constexpr int nf = 2, n_anc = 2, n_rel = 3; static constexpr int fa[3] = {0, 1, 0}, fr[3] = {0, 1, 0}; };
-template <> struct Shape<QPI> { static constexpr int nf = 2, n_anc = 2, n_rel = 3; static constexpr int fa[3] = {0, 1, 0}, fr[3] = {0, 2, 0}; };
-template <> struct Shape<Q2U> { static constexpr int nf = 2, n_anc = 2, n_rel = 2; static constexpr int fa[3] = {0, 1, 0}, fr[3] = {0, 1, 0}; };
-template <> struct Shape<QUP> { static constexpr int nf = 2, n_anc = 2, n_rel = 3; static constexpr int fa[3] = {0, 1, 0}, fr[3] = {0, 1, 0}; };
 
-// Lane-level test of candidate c.  Returns ST_NON / ST_ANS, or ST_PEND with
-// *seg = the backward list a wavefront must intersect.
-template <int QT, class T>
-__device__ __forceinline__ int32_t lane_test(const GraphView& g, const FSet* F, const int32_t* rel,
-                                             int32_t c, int2* seg, T& tl)
+// --------------------------------------------------------------- negatives
+// Bidirectional rejection sampling of the negatives, in rounds of candidate
+// draws.  Per round:
+//   k_candidates  one lane per (query, draw): the draw, its cheap checks,
+//                 and either a decision or a push to the heavy queue;
+//   k_heavy       one wavefront per queued (query, draw): intersection of a
+//                 long backward list with the forward-cached list(s);
+//   k_compact     one workgroup per query: first-occurrence test of every
+//                 draw so far, ordered selection of the first n_neg kept.
+// Queries still short of n_neg after a round go to the next round through a
+// device-side list, so rounds need no host synchronisation.
+
+// Lists per shape (anchor slot, relation slot) at the cut the planner picks:
+//   1p {a0}, 2p/3p {V1}, 2i/3i/2u {anchors}, ip/up {Y0, Y1}, pi {V1, a1}.
+// cached = forward caching to the cut (A_r(a) at a cut node one projection
+// above the anchor); otherwise the list is the anchor's neighbour list used
+// for an edge test at a cut placed on the anchor, which may be decided from
+// either end of the edge.  n_anc / n_rel: slots the shape uses.
+template <int QT> struct Shape;
+#define SHAPE(Q, NF, NA, NR, A0, A1, A2, R0, R1, R2, C0, C1, C2)                                 \
+    template <> struct Shape<Q> {                                                              \
+        static constexpr int nf = NF, n_anc = NA, n_rel = NR;                                  \
+        static constexpr int fa[3] = {A0, A1, A2}, fr[3] = {R0, R1, R2}, cached[3] = {C0, C1, C2}; \
+    };
+SHAPE(Q1P, 1, 1, 1, 0, 0, 0, 0, 0, 0, 0, 0, 0)
+SHAPE(Q2P, 1, 1, 2, 0, 0, 0, 0, 0, 0, 1, 0, 0)
+SHAPE(Q3P, 1, 1, 3, 0, 0, 0, 0, 0, 0, 1, 0, 0)
+SHAPE(Q2I, 2, 2, 2, 0, 1, 0, 0, 1, 0, 0, 0, 0)
+SHAPE(Q3I, 3, 3, 3, 0, 1, 2, 0, 1, 2, 0, 0, 0)
+SHAPE(QIP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
+SHAPE(QPI, 2, 2, 3, 0, 1, 0, 0, 2, 0, 1, 0, 0)
+SHAPE(Q2U, 2, 2, 2, 0, 1, 0, 0, 1, 0, 0, 0, 0)
+SHAPE(QUP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
+#undef SHAPE
+
+constexpr int CWG = 256;         // threads of the candidate and compaction workgroups
+constexpr int HEAVY_WG = 256;    // threads of the heavy-queue workgroups
+constexpr int QF = 8;            // int32 per query in the per-query block
+constexpr int PERSIST_BLOCKS = 2048;
+
+// Workspace carved out of the caller's buffer.
+struct Ws {
+    int32_t* ctrl;    // [0] queue pushes [1] queue pops [2 + k] size of active list k
+    int32_t* qf;      // [B][QF]: list k at [2k, 2k+1) edge range; [6] bit k: list k staged
+    int32_t* cval;    // [B][neg_tries] candidate ids
+    uint8_t* status;  // [B][neg_tries] ST_*
+    int32_t* act[2];  // active query lists
+    int2* queue;      // (query, draw) items
+    int64_t qcap;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Round r covers draws [bound(r-1), bound(r)): first n_neg plus a margin,
+// then doubling, up to neg_tries.
+inline int32_t round_end(const SampleParams& p, int r)
 {
-    if (QT == Q1P) return has(F[0], c, tl) ? ST_ANS : ST_NON;
-    if (QT == Q2I) return (has(F[0], c, tl) && has(F[1], c, tl)) ? ST_ANS : ST_NON;
-    if (QT == Q3I) return (has(F[0], c, tl) && has(F[1], c, tl) && has(F[2], c, tl)) ? ST_ANS : ST_NON;
-    if (QT == Q2U) return (has(F[0], c, tl) || has(F[1], c, tl)) ? ST_ANS : ST_NON;
-    if (QT == QPI && !has(F[1], c, tl)) return ST_NON;   // the one-hop branch fails
+    int64_t e = p.n_neg + p.n_neg / 16 + 32;
+    e = (e + 63) / 64 * 64;
+    for (int k = 0; k < r; ++k) e *= 2;
+    return (int32_t)(e < p.neg_tries ? e : p.neg_tries);
+}
+
+inline int n_rounds(const SampleParams& p)
+{
+    int r = 0;
+    while (round_end(p, r) < p.neg_tries) ++r;
+    return r + 1;
+}
+
+inline int32_t max_round_len(const SampleParams& p)
+{
+    int32_t m = 0, prev = 0;
+    for (int r = 0; r < n_rounds(p); ++r) {
+        const int32_t e = round_end(p, r);
+        m = e - prev > m ? e - prev : m;
+        prev = e;
+    }
+    return m;
+}
+
+size_t ws_layout(const SampleParams& p, Ws* w, char* base)
+{
+    const int64_t B = p.batch, T = p.neg_tries > 0 ? p.neg_tries : 1;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char* ptr = base ? base + off : nullptr;
+        off += align256(bytes);
+        return ptr;
+    };
+    Ws x;
+    x.ctrl = (int32_t*)take(64 * sizeof(int32_t));
+    x.qf = (int32_t*)take((size_t)B * QF * sizeof(int32_t));
+    x.cval = (int32_t*)take((size_t)B * T * sizeof(int32_t));
+    x.status = (uint8_t*)take((size_t)B * T);
+    x.act[0] = (int32_t*)take((size_t)B * sizeof(int32_t));
+    x.act[1] = (int32_t*)take((size_t)B * sizeof(int32_t));
+    x.qcap = B * (int64_t)max_round_len(p);
+    x.queue = (int2*)take((size_t)x.qcap * sizeof(int2));
+    if (w) *w = x;
+    return off;
+}
+
+// Tally of one lane summed over its wavefront and added to the query's
+// counters (the wavefront must be converged).
+template <class T>
+__device__ __forceinline__ void flush_tally(T& tl, int64_t* stats, int32_t b, int lane)
+{
+    if constexpr (T::on) {
+        uint64_t x = tl.b, y = tl.l;
+        for (int s = 32; s > 0; s >>= 1) {
+            x += __shfl_xor(x, s);
+            y += __shfl_xor(y, s);
+        }
+        if (lane == 0 && (x | y)) {
+            atomicAdd((unsigned long long*)&stats[2 * (int64_t)b], (unsigned long long)x);
+            atomicAdd((unsigned long long*)&stats[2 * (int64_t)b + 1], (unsigned long long)y);
+        }
+        tl.b = tl.l = 0;
+    }
+}
+
+// Edges [x, y) of v under r when v's node-pointer pair (n0, n1) is known.
+template <class T>
+__device__ __forceinline__ int2 group_from(const DirView& d, int32_t n0, int32_t n1, int32_t r, T& tl)
+{
+    int32_t lo = n0, hi = n1;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        tl.read(&d.grp[mid].x, 4);
+        if (d.grp[mid].x < r) lo = mid + 1; else hi = mid;
+    }
+    if (lo < n1 && d.grp[lo].x == r) {
+        tl.read(&d.grp[lo].y, 4);
+        tl.read(&d.grp[lo + 1].y, 4);
+        return make_int2(d.grp[lo].y, d.grp[lo + 1].y);
+    }
+    return make_int2(0, 0);
+}
+
+// Is (a, r, c) an edge?  From the anchor's list when it is staged in LDS,
+// otherwise from c's reverse list under r (c's node pair already loaded).
+template <class T>
+__device__ __forceinline__ bool edge_test(const GraphView& g, const FSet& Fa, int32_t a, int32_t r,
+                                          int32_t c, int32_t n0, int32_t n1, T& tl)
+{
+    if (Fa.lds) return has(Fa, c, tl);
+    const int2 s = group_from(g.rev, n0, n1, r, tl);
+    return s.y > s.x && has(g.rev.nbr + s.x, s.y - s.x, a, true, tl);
+}
+
+// Decision for candidate c at lane level: ST_NON, ST_ANS, or ST_PEND when a
+// wavefront must intersect a long list.
+template <int QT, class T>
+__device__ __forceinline__ int32_t cand_test(const GraphView& g, const FSet* F, const int32_t* anc,
+                                             const int32_t* rel, int32_t c, int32_t n0, int32_t n1,
+                                             T& tl)
+{
+    if (QT == Q1P) return edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) ? ST_ANS : ST_NON;
+    if (QT == Q2I)
+        return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) &&
+                edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl)) ? ST_ANS : ST_NON;
+    if (QT == Q3I)
+        return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) &&
+                edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl) &&
+                edge_test(g, F[2], anc[2], rel[2], c, n0, n1, tl)) ? ST_ANS : ST_NON;
+    if (QT == Q2U)
+        return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) ||
+                edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl)) ? ST_ANS : ST_NON;
+    if (QT == QPI && !edge_test(g, F[1], anc[1], rel[2], c, n0, n1, tl)) return ST_NON;
     // backward step from c under the relation entering the root
     const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
-    const int2 s = group_range(g.rev, c, rb, tl);
+    const int2 s = group_from(g.rev, n0, n1, rb, tl);
     if (s.y == s.x) return ST_NON;
-    if (s.y - s.x > LANE_SEG) { *seg = s; return ST_PEND; }
-    tl.read(g.rev.nbr + s.x, 4 * (s.y - s.x));
+    const int32_t ns = s.y - s.x;
+    if (ns > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) return ST_PEND;
+    tl.read(g.rev.nbr + s.x, 4 * ns);
     for (int32_t k = s.x; k < s.y; ++k) {
         const int32_t y = g.rev.nbr[k];
         if (QT == Q2P || QT == QPI) { if (has(F[0], y, tl)) return ST_ANS; }
@@ -290,7 +441,7 @@ __device__ __forceinline__ int32_t lane_test(const GraphView& g, const FSet* F, 
         else if (QT == QUP) { if (has(F[0], y, tl) || has(F[1], y, tl)) return ST_ANS; }
         else {  // 3p: second backward step from y under r1
             const int2 s2 = group_range(g.rev, y, rel[1], tl);
-            if (s2.y - s2.x > LANE_SEG) { *seg = s; return ST_PEND; }
+            if (s2.y - s2.x > LANE_SEG) return ST_PEND;
             tl.read(g.rev.nbr + s2.x, 4 * (s2.y - s2.x));
             for (int32_t m = s2.x; m < s2.y; ++m)
                 if (has(F[0], g.rev.nbr[m], tl)) return ST_ANS;
@@ -299,18 +450,23 @@ __device__ __forceinline__ int32_t lane_test(const GraphView& g, const FSet* F, 
     return ST_NON;
 }
 
-// Wavefront-level test of a queued candidate whose backward list is s.
+// Wavefront decision for a queued candidate (the one-hop branch of pi has
+// already passed at lane level).
 template <int QT, class T>
-__device__ bool wave_test(const GraphView& g, const FSet* F, const int32_t* rel, int2 s, int lane,
-                          T& tl)
+__device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel, int32_t c, int lane,
+                           T& tl)
 {
+    const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
+    int2 s = group_range(g.rev, c, rb, tl);   // same address in every lane
+    s.x = uni(s.x);
+    s.y = uni(s.y);
     const int32_t* S = g.rev.nbr + s.x;
     const int32_t ns = s.y - s.x;
-    if (QT == Q2P || QT == QPI) return wave_meet(S, ns, true, F[0].p, F[0].n, !F[0].lds, lane, tl);
+    if (QT == Q2P || QT == QPI) return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl);
     if (QT == QIP) return wave_meet3(S, ns, F[0], F[1], lane, tl);
     if (QT == QUP)
-        return wave_meet(S, ns, true, F[0].p, F[0].n, !F[0].lds, lane, tl) ||
-               wave_meet(S, ns, true, F[1].p, F[1].n, !F[1].lds, lane, tl);
+        return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl) ||
+               wave_meet(S, ns, true, F[1].p, F[1].n, false, lane, tl);
     if (QT == Q3P) {
         for (int32_t k = 0; k < ns; k += 64) {
             if (lane == 0) tl.read(S + k, 4 * min(64, ns - k));
@@ -320,14 +476,164 @@ __device__ bool wave_test(const GraphView& g, const FSet* F, const int32_t* rel,
             while (todo) {
                 const int src = __ffsll((unsigned long long)todo) - 1;
                 todo &= todo - 1;
-                const int32_t x = __shfl(s2.x, src), y = __shfl(s2.y, src);
-                if (wave_meet(g.rev.nbr + x, y - x, true, F[0].p, F[0].n, !F[0].lds, lane, tl))
-                    return true;
+                const int32_t x = uni(__shfl(s2.x, src)), y = uni(__shfl(s2.y, src));
+                if (wave_meet(g.rev.nbr + x, y - x, true, F[0].p, F[0].n, false, lane, tl)) return true;
             }
         }
         return false;
     }
     return false;
+}
+
+__device__ __forceinline__ bool query_ok(const GraphView& g, const smore_sample_out& out, int32_t b,
+                                         int n_anc, int n_rel, int32_t R, int32_t* anc, int32_t* rel)
+{
+    bool ok = out.positive[b] >= 0;
+    for (int k = 0; k < 3; ++k) {
+        rel[k] = out.relations[3 * (int64_t)b + k];
+        anc[k] = out.anchors[3 * (int64_t)b + k];
+        if (k < n_rel && (rel[k] < 0 || rel[k] >= R)) ok = false;
+        if (k < n_anc && (anc[k] < 0 || anc[k] >= g.V)) ok = false;
+    }
+    return ok;
+}
+
+// Per query: validity, forward-cached lists, staging plan, active list.
+template <int QT, class T>
+__global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, smore_sample_out out,
+                                                 Ws ws, int64_t* stats, int32_t R)
+{
+    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= p.batch) return;
+    int32_t anc[3], rel[3];
+    int32_t* row = out.negatives + (int64_t)b * p.n_neg;
+    if (stats) { stats[2 * (int64_t)b] = 0; stats[2 * (int64_t)b + 1] = 0; }
+    if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
+        for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
+        out.n_valid[b] = -1;
+        out.neg_draws[b] = -1;
+        return;
+    }
+    if (p.n_neg == 0) {
+        out.n_valid[b] = 0;
+        out.neg_draws[b] = 0;
+        return;
+    }
+    T tl;
+    int32_t* q = ws.qf + (int64_t)b * QF;
+    int32_t used = 0, staged = 0;
+    for (int f = 0; f < Shape<QT>::nf; ++f) {
+        const int2 r = group_range(g.fwd, anc[Shape<QT>::fa[f]], rel[Shape<QT>::fr[f]], tl);
+        q[2 * f] = r.x;
+        q[2 * f + 1] = r.y;
+        const int32_t n = r.y - r.x;
+        if (n <= STAGE - used) {
+            staged |= 1 << f;
+            used += n;
+        }
+        // forward caching reads the list once; a staged anchor list too
+        if (Shape<QT>::cached[f] || (staged >> f & 1)) tl.read(g.fwd.nbr + r.x, 4 * n);
+    }
+    q[6] = staged;
+    ws.act[0][atomicAdd(&ws.ctrl[2], 1)] = b;
+    if constexpr (T::on) {
+        stats[2 * (int64_t)b] = (int64_t)tl.b;
+        stats[2 * (int64_t)b + 1] = (int64_t)tl.l;
+    }
+}
+
+// One workgroup item = (active query, tile of CWG draws of this round).
+template <int QT, class T>
+__global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p, smore_sample_out out,
+                                                    Ws ws, int64_t* stats, int cur, int32_t j0,
+                                                    int32_t j1)
+{
+    __shared__ int32_t stage[STAGE];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int32_t ntiles = (j1 - j0 + CWG - 1) / CWG;
+    const int64_t nitems = (int64_t)uni(ws.ctrl[2 + cur]) * ntiles;
+    T tl;
+    for (int64_t item = blockIdx.x; item < nitems; item += gridDim.x) {
+        const int32_t b = uni(ws.act[cur][item / ntiles]);
+        const int32_t j = j0 + (int32_t)(item % ntiles) * CWG + tid;
+        const bool live = j < j1;
+        const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
+        int32_t c = 0, n0 = 0, n1 = 0;
+        if (live) {
+            c = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
+            n0 = g.rev.node[c];          // every shape starts from c's reverse groups
+            n1 = g.rev.node[c + 1];
+        }
+        int32_t anc[3], rel[3];
+        for (int k = 0; k < 3; ++k) {
+            anc[k] = uni(out.anchors[3 * (int64_t)b + k]);
+            rel[k] = uni(out.relations[3 * (int64_t)b + k]);
+        }
+        const int32_t* qb = ws.qf + (int64_t)b * QF;
+        const int32_t staged = uni(qb[6]);
+        FSet F[3];
+        int32_t used = 0;
+#pragma unroll
+        for (int f = 0; f < 3; ++f) {
+            if (f >= Shape<QT>::nf) { F[f] = FSet{nullptr, 0, true}; continue; }
+            const int32_t beg = uni(qb[2 * f]), n = uni(qb[2 * f + 1]) - beg;
+            if (staged >> f & 1) {
+                for (int32_t k = tid; k < n; k += CWG) stage[used + k] = g.fwd.nbr[beg + k];
+                F[f] = FSet{stage + used, n, true};
+                used += n;
+            } else {
+                F[f] = FSet{g.fwd.nbr + beg, n, false};
+            }
+        }
+        __syncthreads();
+        if (live) {
+            tl.read(g.rev.node + c, 8);
+            const int32_t st = cand_test<QT>(g, F, anc, rel, c, n0, n1, tl);
+            const int64_t at = (int64_t)b * p.neg_tries + j;
+            ws.cval[at] = c;
+            ws.status[at] = (uint8_t)st;
+            if (st == ST_PEND) {
+                const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers every draw of a round
+                ws.queue[slot] = make_int2(b, j);
+            }
+        }
+        flush_tally(tl, stats, b, lane);
+        __syncthreads();   // the next item restages the lists
+    }
+}
+
+// Persistent wavefronts draining the heavy queue.
+template <int QT, class T>
+__global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p, smore_sample_out out,
+                                                    Ws ws, int64_t* stats)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t total = uni(__atomic_load_n(&ws.ctrl[0], __ATOMIC_RELAXED));
+    T tl;
+    // every pass pops one item or leaves, so total + 1 passes always suffice;
+    // the popped index is made wave-uniform so the wave stays converged
+    for (int32_t pass = 0; pass <= total; ++pass) {
+        int32_t idx = 0;
+        if (lane == 0) idx = atomicAdd(&ws.ctrl[1], 1);
+        idx = uni(__shfl(idx, 0));
+        if (idx >= total) break;
+        const int2 it = ws.queue[idx];
+        const int32_t b = uni(it.x), j = uni(it.y);
+        const int64_t at = (int64_t)b * p.neg_tries + j;
+        const int32_t c = uni(ws.cval[at]);
+        int32_t rel[3];
+        for (int k = 0; k < 3; ++k) rel[k] = uni(out.relations[3 * (int64_t)b + k]);
+        const int32_t* qb = ws.qf + (int64_t)b * QF;
+        FSet F[3];
+#pragma unroll
+        for (int f = 0; f < 3; ++f) {
+            const int32_t beg = uni(qb[2 * f]), end = uni(qb[2 * f + 1]);
+            F[f] = f < Shape<QT>::nf ? FSet{g.fwd.nbr + beg, end - beg, false} : FSet{nullptr, 0, true};
+        }
+        const bool ans = heavy_test<QT>(g, F, rel, c, lane, tl);
+        if (lane == 0) ws.status[at] = ans ? ST_ANS : ST_NON;
+        flush_tally(tl, stats, b, lane);
+    }
 }
 
 __device__ __forceinline__ void ht_insert(int32_t* tv, int32_t* tj, uint32_t mask, int shift,
@@ -352,203 +658,141 @@ __device__ __forceinline__ int32_t ht_first(const int32_t* tv, const int32_t* tj
     return tj[h];
 }
 
-template <int QT, class T>
-__global__ __launch_bounds__(WG) void k_verify(GraphView g, SampleParams p, smore_sample_out out,
-                                               int64_t* stats, int32_t tcap, int tshift,
-                                               int32_t R)
+// Per active query: keep draw j iff it is not an answer and no earlier draw
+// has the same value; the first n_neg kept, in draw order, are the
+// negatives.  Queries that are neither complete nor out of budget go to the
+// next round's list.
+__global__ __launch_bounds__(CWG) void k_compact(SampleParams p, smore_sample_out out, Ws ws, int cur,
+                                                 int32_t j_end, int last, int32_t tcap, int tshift)
 {
     extern __shared__ int32_t lds[];
-    int32_t* tv = lds;                  // hash table: candidate value
-    int32_t* tj = tv + tcap;            // hash table: smallest draw index of that value
-    int32_t* stage = tj + tcap;         // staged forward lists
-    int32_t* cval = stage + STAGE;      // candidates of the round
-    int32_t* cst = cval + CHMAX;        // their status
-    int32_t* qi = cst + CHMAX;          // queue: candidate index
-    int2* qs = (int2*)(qi + CHMAX);     // queue: backward list
-    __shared__ int32_t s_f[3][2];
-    __shared__ int32_t s_qlen;
-    __shared__ int32_t s_cnt[NW];
-    __shared__ unsigned long long s_tally[2];
-
+    int32_t* tv = lds;
+    int32_t* tj = lds + tcap;
+    __shared__ int32_t s_cnt[CWG / 64];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int32_t b = blockIdx.x;
-    const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
-    int32_t* negrow = out.negatives + (int64_t)b * p.n_neg;
-    int32_t rel[3], anc[3];
-    bool valid = out.positive[b] >= 0;
-    for (int k = 0; k < 3; ++k) {
-        rel[k] = out.relations[3 * (int64_t)b + k];
-        anc[k] = out.anchors[3 * (int64_t)b + k];
-        // ids the shape uses must index the graph (rows built by a caller)
-        if (k < Shape<QT>::n_rel && (rel[k] < 0 || rel[k] >= R)) valid = false;
-        if (k < Shape<QT>::n_anc && (anc[k] < 0 || anc[k] >= g.V)) valid = false;
-    }
-    if (!valid) {                                      // no query to verify
-        for (int32_t k = tid; k < p.n_neg; k += WG) negrow[k] = -1;
-        if (tid == 0) {
-            out.n_valid[b] = -1;
-            out.neg_draws[b] = -1;
-            if (stats) { stats[2 * (int64_t)b] = 0; stats[2 * (int64_t)b + 1] = 0; }
-        }
-        return;
-    }
-    if (p.n_neg == 0) {
-        if (tid == 0) {
-            out.n_valid[b] = 0;
-            out.neg_draws[b] = 0;
-            if (stats) { stats[2 * (int64_t)b] = 0; stats[2 * (int64_t)b + 1] = 0; }
-        }
-        return;
-    }
-    T tl;
-    // forward caching: the anchors' neighbour lists at the cut
-    constexpr int NF = Shape<QT>::nf;
-    if (tid < NF) {
-        const int2 r = group_range(g.fwd, anc[Shape<QT>::fa[tid]], rel[Shape<QT>::fr[tid]], tl);
-        s_f[tid][0] = r.x;
-        s_f[tid][1] = r.y;
-    }
-    if (tid < 2) s_tally[tid] = 0;
-    for (int32_t k = tid; k < tcap; k += WG) { tv[k] = -1; tj[k] = INT_MAX; }
-    __syncthreads();
-    FSet F[3];
-    int32_t used = 0;
-#pragma unroll
-    for (int f = 0; f < 3; ++f) {
-        if (f >= NF) { F[f] = FSet{nullptr, 0, true}; continue; }
-        const int32_t beg = s_f[f][0], n = s_f[f][1] - s_f[f][0];
-        if (n <= STAGE - used) {
-            for (int32_t k = tid; k < n; k += WG) stage[used + k] = g.fwd.nbr[beg + k];
-            if (tid == 0) tl.read(g.fwd.nbr + beg, 4 * n);
-            F[f] = FSet{stage + used, n, true};
-            used += n;
-        } else {
-            F[f] = FSet{g.fwd.nbr + beg, n, false};
-        }
-    }
-    __syncthreads();
-
     const uint32_t tmask = (uint32_t)tcap - 1;
-    int32_t acc = 0;
-    for (int32_t j0 = 0; acc < p.n_neg && j0 < p.neg_tries;) {
-        const int32_t need = p.n_neg - acc;
-        int32_t ch = ((need + need / 8 + 16 + 63) / 64) * 64;
-        ch = min(ch, CHMAX);
-        ch = min(ch, p.neg_tries - j0);
-        // draw and register in the first-occurrence table
-        for (int32_t i = tid; i < ch; i += WG) {
-            const int32_t c = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)(j0 + i)),
-                                                    (uint32_t)g.V);
-            cval[i] = c;
-            ht_insert(tv, tj, tmask, tshift, c, j0 + i);
-        }
-        if (tid == 0) s_qlen = 0;
+    const int32_t nact = uni(ws.ctrl[2 + cur]);
+    for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
+        const int32_t b = uni(ws.act[cur][qi]);
+        const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
+        const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
+        int32_t* row = out.negatives + (int64_t)b * p.n_neg;
+        for (int32_t k = tid; k < tcap; k += CWG) { tv[k] = -1; tj[k] = INT_MAX; }
         __syncthreads();
-        // lane-level verification of first occurrences
-        for (int32_t i = tid; i < ch; i += WG) {
-            const int32_t c = cval[i];
-            int32_t st;
-            if (ht_first(tv, tj, tmask, tshift, c) != j0 + i) {
-                st = ST_DUP;
-            } else {
-                int2 s;
-                st = lane_test<QT>(g, F, rel, c, &s, tl);
-                if (st == ST_PEND) {
-                    const int32_t slot = atomicAdd(&s_qlen, 1);
-                    qi[slot] = i;
-                    qs[slot] = s;
-                }
+        for (int32_t j = tid; j < j_end; j += CWG) ht_insert(tv, tj, tmask, tshift, cv[j], j);
+        __syncthreads();
+        int32_t acc = 0;
+        for (int32_t row0 = 0; row0 < j_end && acc < p.n_neg; row0 += CWG) {
+            const int32_t j = row0 + tid;
+            int32_t c = 0;
+            bool keep = false;
+            if (j < j_end) {
+                c = cv[j];
+                keep = sv[j] == ST_NON && ht_first(tv, tj, tmask, tshift, c) == j;
             }
-            cst[i] = st;
-        }
-        __syncthreads();
-        // wavefront-level verification of long backward lists
-        const int32_t nq = s_qlen;
-        for (int32_t it = w; it < nq; it += NW) {
-            const bool ans = wave_test<QT>(g, F, rel, qs[it], lane, tl);
-            if (lane == 0) cst[qi[it]] = ans ? ST_ANS : ST_NON;
-        }
-        __syncthreads();
-        // keep non-answers in draw order
-        for (int32_t row = 0; row < ch; row += WG) {
-            const int32_t i = row + tid;
-            const bool keep = i < ch && cst[i] == ST_NON;
             const uint64_t m = __ballot(keep);
             if (lane == 0) s_cnt[w] = __popcll(m);
             __syncthreads();
             int32_t before = acc, total = 0;
-            for (int ww = 0; ww < NW; ++ww) {
+            for (int ww = 0; ww < CWG / 64; ++ww) {
                 if (ww < w) before += s_cnt[ww];
                 total += s_cnt[ww];
             }
             const int32_t rank = before + __popcll(m & lanes_below(lane));
             if (keep && rank < p.n_neg) {
-                negrow[rank] = cval[i];
-                if (rank == p.n_neg - 1) out.neg_draws[b] = j0 + i + 1;
+                row[rank] = c;
+                if (rank == p.n_neg - 1) out.neg_draws[b] = j + 1;
             }
-            acc = min(p.n_neg, acc + total);
+            acc = uni(min(p.n_neg, acc + total));
             __syncthreads();
         }
-        j0 += ch;
-    }
-    for (int32_t k = acc + tid; k < p.n_neg; k += WG) negrow[k] = -1;
-    if (tid == 0) {
-        out.n_valid[b] = acc;
-        if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
-    }
-    if constexpr (T::on) {
-        atomicAdd(&s_tally[0], (unsigned long long)tl.b);
-        atomicAdd(&s_tally[1], (unsigned long long)tl.l);
-        __syncthreads();
-        if (tid == 0) {
-            stats[2 * (int64_t)b] = (int64_t)s_tally[0];
-            stats[2 * (int64_t)b + 1] = (int64_t)s_tally[1];
+        if (acc == p.n_neg || last) {
+            for (int32_t k = acc + tid; k < p.n_neg; k += CWG) row[k] = -1;
+            if (tid == 0) {
+                out.n_valid[b] = acc;
+                if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
+            }
+        } else if (tid == 0) {
+            ws.act[cur ^ 1][atomicAdd(&ws.ctrl[2 + (cur ^ 1)], 1)] = b;
         }
+        __syncthreads();
     }
 }
 
-size_t verify_lds_bytes(int32_t tcap)
+// Resets the queue counters and the next round's list size.
+__global__ void k_round_begin(Ws ws, int nxt)
 {
-    return ((size_t)2 * tcap + STAGE + 5 * CHMAX) * sizeof(int32_t);
+    ws.ctrl[0] = 0;
+    ws.ctrl[1] = 0;
+    ws.ctrl[2 + nxt] = 0;
 }
 
-template <int QT, class T>
-int launch_verify(const GraphView& gv, const SampleParams& p, const smore_sample_out& out,
-                  int64_t* stats, int32_t R, hipStream_t st, const char** err)
+__global__ void k_init(Ws ws)
 {
-    int32_t tcap = 64;
-    while (tcap < 2 * p.neg_tries) tcap <<= 1;
-    int tshift = 32;
-    for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
-    // more than 64 KiB of LDS per workgroup must be requested explicitly
-    static bool attr_set = false;
-    if (verify_lds_bytes(tcap) > 65536 && !attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_verify<QT, T>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)verify_lds_bytes(2 * SMORE_MAX_NEG_TRIES));
-        if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
-        attr_set = true;
-    }
-    k_verify<QT, T><<<p.batch, WG, verify_lds_bytes(tcap), st>>>(gv, p, out, stats, tcap, tshift, R);
-    hipError_t e = hipGetLastError();
+    for (int k = threadIdx.x; k < 64; k += blockDim.x) ws.ctrl[k] = 0;
+}
+
+inline int check_launch(const char** err)
+{
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
     return SMORE_OK;
 }
 
+template <int QT, class T>
+int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample_out& out, Ws ws,
+                  int64_t* stats, int32_t R, hipStream_t st, const char** err)
+{
+    int rc;
+    k_init<<<1, 64, 0, st>>>(ws);
+    k_prepare<QT, T><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, out, ws, stats, R);
+    if ((rc = check_launch(err))) return rc;
+    if (p.n_neg == 0) return SMORE_OK;
+    const int rounds = n_rounds(p);
+    int32_t prev = 0;
+    for (int r = 0; r < rounds; ++r) {
+        const int cur = r & 1;
+        const int32_t j_end = round_end(p, r);
+        k_round_begin<<<1, 1, 0, st>>>(ws, cur ^ 1);
+        k_candidates<QT, T><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
+        if ((rc = check_launch(err))) return rc;
+        k_heavy<QT, T><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats);
+        if ((rc = check_launch(err))) return rc;
+        int32_t tcap = 64;
+        while (tcap < 2 * j_end) tcap <<= 1;
+        int tshift = 32;
+        for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
+        const size_t lds = (size_t)2 * tcap * sizeof(int32_t);
+        static bool attr = false;
+        if (lds > 65536 && !attr) {
+            const hipError_t e = hipFuncSetAttribute((const void*)k_compact,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     (int)(4 * 2 * SMORE_MAX_NEG_TRIES * sizeof(int32_t)));
+            if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
+            attr = true;
+        }
+        k_compact<<<PERSIST_BLOCKS, CWG, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
+                                                    tshift);
+        if ((rc = check_launch(err))) return rc;
+        prev = j_end;
+    }
+    return SMORE_OK;
+}
+
 template <class T>
-int dispatch_verify(QType qt, const GraphView& gv, const SampleParams& p, const smore_sample_out& out,
-                    int64_t* stats, int32_t R, hipStream_t st, const char** err)
+int dispatch_negatives(QType qt, const GraphView& gv, const SampleParams& p, const smore_sample_out& out,
+                       Ws ws, int64_t* stats, int32_t R, hipStream_t st, const char** err)
 {
     switch (qt) {
-        case Q1P: return launch_verify<Q1P, T>(gv, p, out, stats, R, st, err);
-        case Q2P: return launch_verify<Q2P, T>(gv, p, out, stats, R, st, err);
-        case Q3P: return launch_verify<Q3P, T>(gv, p, out, stats, R, st, err);
-        case Q2I: return launch_verify<Q2I, T>(gv, p, out, stats, R, st, err);
-        case Q3I: return launch_verify<Q3I, T>(gv, p, out, stats, R, st, err);
-        case QIP: return launch_verify<QIP, T>(gv, p, out, stats, R, st, err);
-        case QPI: return launch_verify<QPI, T>(gv, p, out, stats, R, st, err);
-        case Q2U: return launch_verify<Q2U, T>(gv, p, out, stats, R, st, err);
-        case QUP: return launch_verify<QUP, T>(gv, p, out, stats, R, st, err);
+        case Q1P: return run_negatives<Q1P, T>(gv, p, out, ws, stats, R, st, err);
+        case Q2P: return run_negatives<Q2P, T>(gv, p, out, ws, stats, R, st, err);
+        case Q3P: return run_negatives<Q3P, T>(gv, p, out, ws, stats, R, st, err);
+        case Q2I: return run_negatives<Q2I, T>(gv, p, out, ws, stats, R, st, err);
+        case Q3I: return run_negatives<Q3I, T>(gv, p, out, ws, stats, R, st, err);
+        case QIP: return run_negatives<QIP, T>(gv, p, out, ws, stats, R, st, err);
+        case QPI: return run_negatives<QPI, T>(gv, p, out, ws, stats, R, st, err);
+        case Q2U: return run_negatives<Q2U, T>(gv, p, out, ws, stats, R, st, err);
+        case QUP: return run_negatives<QUP, T>(gv, p, out, ws, stats, R, st, err);
         default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
     }
 }
@@ -566,21 +810,31 @@ GraphView view_of(const smore_graph* g)
 
 }  // namespace
 
+size_t negatives_workspace_bytes(const SampleParams& p)
+{
+    return ws_layout(p, nullptr, nullptr);
+}
+
 int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
                     const smore_sample_out& out, hipStream_t st, const char** err)
 {
     k_positive<<<(p.batch + 255) / 256, 256, 0, st>>>(view_of(g), wp, p, out);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
-    return SMORE_OK;
+    return check_launch(err);
 }
 
 int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
-                    const smore_sample_out& out, int64_t* stats, hipStream_t st, const char** err)
+                    const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
+                    hipStream_t st, const char** err)
 {
+    Ws ws;
+    const size_t need = ws_layout(p, &ws, (char*)workspace);
+    if (!workspace || ws_bytes < need) {
+        *err = "workspace too small (see smore_sample_workspace_bytes)";
+        return SMORE_E_INVALID_ARG;
+    }
     const GraphView gv = view_of(g);
-    if (stats) return dispatch_verify<Tally>(qt, gv, p, out, stats, g->R, st, err);
-    return dispatch_verify<NoTally>(qt, gv, p, out, nullptr, g->R, st, err);
+    if (stats) return dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, st, err);
+    return dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
 }
 
 }  // namespace smore

@@ -70,6 +70,7 @@ int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_
 int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
                     const smore_sample_out& out, hipStream_t stream, const char** err);
 int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
-                    const smore_sample_out& out, int64_t* stats, hipStream_t stream,
-                    const char** err);
+                    const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
+                    hipStream_t stream, const char** err);
+size_t negatives_workspace_bytes(const SampleParams& p);
 }  // namespace smore

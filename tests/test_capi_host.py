@@ -211,3 +211,16 @@ def test_build_graph_validation_on_host(L):
     _expect(L.smore_build_graph(tr, 2**31, 2, 1, 0, ctypes.byref(g)), -6)
     _expect(L.smore_build_graph(tr, 2**30, 2, 1, sm.ADD_INVERSE, ctypes.byref(g)), -6)
     assert not g.value
+
+
+def test_workspace_bytes(L):
+    dag = sm.query_preset("3p")
+    small = sm.workspace_bytes(dag, sm.make_args(16, 8))
+    big = sm.workspace_bytes(dag, sm.make_args(16384, 512))
+    assert 0 < small < big
+    # grows with batch x neg_tries (per-draw ids and states at least)
+    assert big >= 16384 * 2048 * 5
+    bad = sm.make_args(4, 2)
+    bad.neg_tries = 1
+    n = ctypes.c_size_t()
+    _expect(L.smore_sample_workspace_bytes(None, ctypes.byref(dag), ctypes.byref(bad), ctypes.byref(n)), -1)

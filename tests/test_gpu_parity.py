@@ -176,3 +176,45 @@ def test_sample_parity_large_sampled_rows(name):
         rows = np.sort(rng.choice(cfg.batch, 96, replace=False))
         ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
         assert_same(got, ref, rows=rows, what=f"{name}/{qt}")
+
+
+@pytest.mark.parametrize("qt", sm.TYPES)
+def test_accounting_variant_and_stage_split(qt):
+    # the read-accounting build and the two-stage calls return the same rows
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    full = gpu_sample(g, qt, 300, 40, seed=4)
+    dag = sm.query_preset(qt)
+    args = sm.make_args(300, 40, seed=4)
+    out = sm.alloc_outputs(300, 40)
+    sm.sample_positives(g, dag, args, out)
+    stats = torch.zeros((300, 2), dtype=torch.int64, device="cuda")
+    sm.sample_negatives(g, dag, args, out, stats)
+    got = to_numpy(out)
+    for k in full:
+        assert np.array_equal(full[k], got[k]), k
+    st = stats.cpu().numpy()
+    ok = got["n_valid"] >= 0
+    assert (st[ok] > 0).all() and (st[~ok] == 0).all() and (st[:, 1] * 64 >= st[:, 0] // 8).all()
+
+
+def test_negatives_on_caller_queries():
+    # rows with an id out of range are skipped, the others verified
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations)
+    ref = og.sample("2p", 64, 20, seed=2)
+    dag = sm.query_preset("2p")
+    args = sm.make_args(64, 20, seed=2)
+    out = {k: torch.from_numpy(np.ascontiguousarray(v)).cuda() for k, v in ref.items()}
+    out["anchors"][5, 0] = cfg.n_entities          # out of range
+    out["relations"][6, 1] = -7                     # out of range
+    out["negatives"].fill_(123)
+    sm.sample_negatives(g, dag, args, out)
+    got = to_numpy(out)
+    keep = np.ones(64, bool)
+    keep[[5, 6]] = False
+    for k in ("negatives", "n_valid", "neg_draws"):
+        assert np.array_equal(got[k][keep], ref[k][keep]), k
+    assert (got["n_valid"][[5, 6]] == -1).all() and (got["negatives"][[5, 6]] == -1).all()

@@ -1,0 +1,47 @@
+"""Parity at full size on the Freebase-shaped graph (86M entities, 338M
+triples), in the launch configuration bench.py times: the whole batch of
+16,384 queries x 512 negatives runs on the GPU; the oracle recomputes a
+random sample of rows one query at a time (its exhaustive answer sets make
+every query cost up to seconds here).  Also checks that the read-accounting
+variant of the verification kernel returns the same rows."""
+import numpy as np
+import pytest
+
+from gpu_common import (FIELDS, assert_same, config_graph, graph_pair, oracle_rows, progress,
+                        require_gpu, to_numpy)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.timeout(900)
+def test_freebase_sampled_rows_and_accounting():
+    require_gpu()
+    import torch
+
+    import paper_2110_14890_amd as sm
+
+    progress("generating the Freebase-shaped graph")
+    cfg, tr = config_graph("freebase")
+    progress(f"{len(tr):,} triples; building device and oracle graphs")
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
+    del tr
+    rng = np.random.default_rng(1)
+    for qt in cfg.query_types:
+        dag = sm.query_preset(qt)
+        args = sm.make_args(cfg.batch, cfg.n_neg, seed=cfg.seed)
+        out = sm.alloc_outputs(cfg.batch, cfg.n_neg)
+        sm.sample_positives(g, dag, args, out)
+        sm.sample_negatives(g, dag, args, out)
+        got = to_numpy(out)
+        stats = torch.zeros((cfg.batch, 2), dtype=torch.int64, device="cuda")
+        sm.sample_negatives(g, dag, args, out, stats)
+        counted = to_numpy(out)
+        for k in FIELDS:
+            assert np.array_equal(got[k], counted[k]), k
+        st = stats.cpu().numpy()
+        assert (st >= 0).all() and (st[got["n_valid"] >= 0, 0] > 0).all()
+        rows = np.sort(rng.choice(cfg.batch, 24, replace=False))
+        progress(f"{qt}: oracle on {len(rows)} sampled rows")
+        ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
+        assert_same(got, ref, rows=rows, what=f"freebase/{qt}")
+        progress(f"{qt}: ok, {int((got['n_valid'] == cfg.n_neg).sum())} complete queries")
