@@ -193,15 +193,18 @@ def main():
     # dominant kernel: the verification kernel with the largest time
     dom = max(types, key=lambda qt: per_type[qt]["verify_ms"])
     d = per_type[dom]
-    achieved = d["verify_line_GBps"]
+    achieved = d["verify_useful_GBps"]
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 5), "traffic": None,
-                "kernel": f"k_verify<{dom}>",
-                "bytes_per_launch": acct[dom]["lines"] * 64,
+                "kernel": f"negative sampling of {dom} (smore_sample_negatives)",
+                "bytes_per_launch": acct[dom]["bytes"],
+                "bytes_per_query": round(acct[dom]["bytes"] / max(acct[dom]["valid"], 1), 1),
                 "avg_launch_ms": round(d["verify_ms"], 4),
-                "accounting": "64-byte lines spanned by each graph read of the verification "
-                              "(node pointers, relation-search probes, group bounds, neighbour "
-                              "lists, out-of-LDS forward lists), summed per launch"}
+                "accounting": "graph bytes the verification reads per query: forward-cached "
+                              "lists once, then per candidate draw its reverse node pointers, "
+                              "relation-search probes, group bounds and backward lists (and the "
+                              "searches into long lists); lookups inside forward-cached lists "
+                              "are not counted"}
 
     cpu = None
     if not args.no_cpu_baseline:

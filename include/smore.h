@@ -118,7 +118,9 @@ int smore_graph_info(const smore_graph *g, int64_t *n_entities, int64_t *n_relat
    inspection).  which: 0 fwd node_ptr [V+1], 1 fwd groups [2*(S_fwd+1)]
    (relation, first edge) pairs, 2 fwd neighbours [E], 3 rev node_ptr,
    4 rev groups, 5 rev neighbours, 6 active_in (entities with an in-edge,
-   ascending).  count must equal the array length.  Synchronous. */
+   ascending), 7 in-edge mask [(V+31)/32] (bit v % 32 of word v / 32 set
+   iff entity v has an in-edge).  count must equal the array length.
+   Synchronous. */
 int smore_graph_copy(const smore_graph *g, int32_t which, int32_t *host_dst, int64_t count);
 
 /* Fill *out with one of the nine negation-free shapes "1p" "2p" "3p" "2i"

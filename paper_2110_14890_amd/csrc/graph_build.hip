@@ -237,6 +237,19 @@ __global__ void k_compact_active(const int32_t* __restrict__ node, int32_t V,
     if (v < V && node[v + 1] > node[v]) out[pos[v]] = (int32_t)v;
 }
 
+// bit v of the mask: entity v has at least one in-edge
+__global__ void k_has_in(const int32_t* __restrict__ node, int32_t V, uint32_t* __restrict__ bits)
+{
+    const int64_t w = (int64_t)blockIdx.x * BT + threadIdx.x;
+    if (w * 32 >= V) return;
+    uint32_t word = 0;
+    for (int b = 0; b < 32; ++b) {
+        const int64_t v = w * 32 + b;
+        if (v < V && node[v + 1] > node[v]) word |= 1u << b;
+    }
+    bits[w] = word;
+}
+
 inline unsigned grid_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // Owns temporary device buffers for the duration of a build.
@@ -476,9 +489,13 @@ int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_
     TRY(hipMalloc(&g->active_in, (size_t)(na > 0 ? na : 1) * 4));
     k_compact_active<<<grid_for(V, BT), BT>>>(g->r_node, V, f, g->active_in);
     TRY(hipGetLastError());
+    const int64_t words = ((int64_t)V + 31) / 32;
+    TRY(hipMalloc(&g->has_in, (size_t)words * 4));
+    k_has_in<<<grid_for(words, BT), BT>>>(g->r_node, V, g->has_in);
+    TRY(hipGetLastError());
     TRY(hipDeviceSynchronize());
     g->n_active = na;
-    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na) * 4 +
+    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na + words) * 4 +
                (size_t)(g->S_fwd + g->S_rev + 2) * sizeof(int2);
     return SMORE_OK;
 }

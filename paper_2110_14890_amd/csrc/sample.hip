@@ -34,7 +34,7 @@ namespace {
 constexpr int WG = 256;       // threads per verify workgroup
 constexpr int NW = WG / 64;   // wavefronts per workgroup
 constexpr int CHMAX = 512;    // candidates per round
-constexpr int STAGE = 2048;   // LDS entries for staged forward lists
+constexpr int STAGE = 1024;   // LDS entries per wavefront for staged forward lists
 constexpr int LANE_SEG = 8;   // backward lists up to this length stay on one lane
 
 enum : int32_t { ST_NON = 0, ST_ANS = 1, ST_DUP = 2, ST_PEND = 3 };
@@ -131,50 +131,94 @@ __device__ __forceinline__ uint64_t lanes_below(int lane)
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Do the sorted lists A and B share an element?  Whole wavefront; the
-// shorter list is read 64 entries at a time and each entry is searched in
-// the longer one.  a_glob / b_glob: whether the list is graph memory.
+// Four independent membership searches of x[0..3] in the sorted list
+// B[0..nb) (nb wave-uniform): branchless, the same number of steps in every
+// lane, and the four loads of a step independent of each other, so a lane
+// keeps four dependent chains in flight.  A key of -1 never matches.
 template <class T>
-__device__ bool wave_meet(const int32_t* A, int32_t na, bool a_glob, const int32_t* B, int32_t nb,
-                          bool b_glob, int lane, T& tl)
+__device__ __forceinline__ void search4(const int32_t* B, int32_t nb, const int32_t* x, bool* found,
+                                        bool count, T& tl)
 {
-    if (na > nb) {
-        const int32_t* t = A; A = B; B = t;
-        const int32_t n = na; na = nb; nb = n;
-        const bool g = a_glob; a_glob = b_glob; b_glob = g;
+    int32_t base[4] = {0, 0, 0, 0};
+    if (nb <= 0) {
+        found[0] = found[1] = found[2] = found[3] = false;
+        return;
     }
-    for (int32_t k = 0; k < na; k += 64) {
-        if (a_glob && lane == 0) tl.read(A + k, 4 * min(64, na - k));
-        const bool hit = k + lane < na && has(B, nb, A[k + lane], b_glob, tl);
-        if (__ballot(hit)) return true;
+    for (int32_t n = nb; n > 1;) {
+        const int32_t half = n >> 1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (count) tl.read(B + base[k] + half, 4);
+            base[k] = B[base[k] + half] <= x[k] ? base[k] + half : base[k];
+        }
+        n -= half;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (count) tl.read(B + base[k], 4);
+        found[k] = B[base[k]] == x[k];
+    }
+}
+
+// Does some element of K[0..nk) occur in L[0..nl)?  Whole wavefront, 256
+// keys per step (four per lane).  k_glob / l_glob: whether reads of the
+// list count as graph traffic.
+template <class T>
+__device__ bool wave_any(const int32_t* K, int32_t nk, bool k_glob, const int32_t* L, int32_t nl,
+                         bool l_glob, int lane, T& tl)
+{
+    for (int32_t k0 = 0; k0 < nk; k0 += 256) {
+        int32_t x[4];
+        bool f[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int32_t i = k0 + 64 * k + lane;
+            x[k] = i < nk ? K[i] : -1;
+        }
+        if (k_glob && lane == 0) tl.read(K + k0, 4 * min(256, nk - k0));
+        search4(L, nl, x, f, l_glob, tl);
+        if (__ballot(f[0] || f[1] || f[2] || f[3])) return true;
     }
     return false;
 }
 
-// Does the sorted graph list S share one element with both A and B?
+// Do the sorted lists A and B share an element?  The shorter is the key
+// list, searched in the longer.
+template <class T>
+__device__ bool wave_meet(const int32_t* A, int32_t na, bool a_glob, const int32_t* B, int32_t nb,
+                          bool b_glob, int lane, T& tl)
+{
+    if (na <= nb) return wave_any(A, na, a_glob, B, nb, b_glob, lane, tl);
+    return wave_any(B, nb, b_glob, A, na, a_glob, lane, tl);
+}
+
+// Does the sorted graph list S share one element with both A and B?  The
+// shortest of the three is the key list, searched in the other two.
 template <class T>
 __device__ bool wave_meet3(const int32_t* S, int32_t ns, FSet A, FSet B, int lane, T& tl)
 {
-    // read the shortest of the three lists, search the other two
-    if (A.n < ns && A.n <= B.n) {
-        for (int32_t k = 0; k < A.n; k += 64) {
-            const bool hit = k + lane < A.n && has(B, A.p[k + lane], tl) &&
-                             has(S, ns, A.p[k + lane], true, tl);
-            if (__ballot(hit)) return true;
-        }
-        return false;
+    const int32_t *K = S, *L1 = A.p, *L2 = B.p;
+    int32_t nk = ns, n1 = A.n, n2 = B.n;
+    bool kg = true, g1 = false, g2 = false;   // lookups inside forward lists are not counted
+    if (A.n < nk && A.n <= B.n) {
+        K = A.p; nk = A.n; kg = false;
+        L1 = S; n1 = ns; g1 = true;
+    } else if (B.n < nk) {
+        K = B.p; nk = B.n; kg = false;
+        L2 = S; n2 = ns; g2 = true;
     }
-    if (B.n < ns) {
-        for (int32_t k = 0; k < B.n; k += 64) {
-            const bool hit = k + lane < B.n && has(A, B.p[k + lane], tl) &&
-                             has(S, ns, B.p[k + lane], true, tl);
-            if (__ballot(hit)) return true;
+    for (int32_t k0 = 0; k0 < nk; k0 += 256) {
+        int32_t x[4];
+        bool f1[4], f2[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int32_t i = k0 + 64 * k + lane;
+            x[k] = i < nk ? K[i] : -1;
         }
-        return false;
-    }
-    for (int32_t k = 0; k < ns; k += 64) {
-        if (lane == 0) tl.read(S + k, 4 * min(64, ns - k));
-        const bool hit = k + lane < ns && has(A, S[k + lane], tl) && has(B, S[k + lane], tl);
+        if (kg && lane == 0) tl.read(K + k0, 4 * min(256, nk - k0));
+        search4(L1, n1, x, f1, g1, tl);
+        search4(L2, n2, x, f2, g2, tl);
+        const bool hit = (f1[0] && f2[0]) || (f1[1] && f2[1]) || (f1[2] && f2[2]) || (f1[3] && f2[3]);
         if (__ballot(hit)) return true;
     }
     return false;
@@ -542,28 +586,34 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     }
 }
 
-// One workgroup item = (active query, tile of CWG draws of this round).
+// One wavefront per active query (persistent over the list, several
+// queries per workgroup and no workgroup barrier): the query's lists are
+// staged once into the wave's LDS slice, then each lane takes DPL draws of
+// the round at a time, issuing all their first loads before deciding them
+// one by one.
+constexpr int DPL = 4;
+
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int QT, class T>
 __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p, smore_sample_out out,
                                                     Ws ws, int64_t* stats, int cur, int32_t j0,
                                                     int32_t j1)
 {
-    __shared__ int32_t stage[STAGE];
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int32_t ntiles = (j1 - j0 + CWG - 1) / CWG;
-    const int64_t nitems = (int64_t)uni(ws.ctrl[2 + cur]) * ntiles;
+    __shared__ int32_t stage_all[CWG / 64][STAGE];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t* stage = stage_all[w];
+    const int32_t nact = uni(ws.ctrl[2 + cur]);
+    const int32_t nwaves = gridDim.x * (CWG / 64);
     T tl;
-    for (int64_t item = blockIdx.x; item < nitems; item += gridDim.x) {
-        const int32_t b = uni(ws.act[cur][item / ntiles]);
-        const int32_t j = j0 + (int32_t)(item % ntiles) * CWG + tid;
-        const bool live = j < j1;
+    for (int32_t qi = uni(blockIdx.x * (CWG / 64) + w); qi < nact; qi += nwaves) {
+        const int32_t b = uni(ws.act[cur][qi]);
         const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
-        int32_t c = 0, n0 = 0, n1 = 0;
-        if (live) {
-            c = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
-            n0 = g.rev.node[c];          // every shape starts from c's reverse groups
-            n1 = g.rev.node[c + 1];
-        }
         int32_t anc[3], rel[3];
         for (int k = 0; k < 3; ++k) {
             anc[k] = uni(out.anchors[3 * (int64_t)b + k]);
@@ -578,27 +628,62 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             if (f >= Shape<QT>::nf) { F[f] = FSet{nullptr, 0, true}; continue; }
             const int32_t beg = uni(qb[2 * f]), n = uni(qb[2 * f + 1]) - beg;
             if (staged >> f & 1) {
-                for (int32_t k = tid; k < n; k += CWG) stage[used + k] = g.fwd.nbr[beg + k];
+                for (int32_t k = lane; k < n; k += 64) stage[used + k] = g.fwd.nbr[beg + k];
                 F[f] = FSet{stage + used, n, true};
                 used += n;
             } else {
                 F[f] = FSet{g.fwd.nbr + beg, n, false};
             }
         }
-        __syncthreads();
-        if (live) {
-            tl.read(g.rev.node + c, 8);
-            const int32_t st = cand_test<QT>(g, F, anc, rel, c, n0, n1, tl);
-            const int64_t at = (int64_t)b * p.neg_tries + j;
-            ws.cval[at] = c;
-            ws.status[at] = (uint8_t)st;
-            if (st == ST_PEND) {
-                const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers every draw of a round
-                ws.queue[slot] = make_int2(b, j);
+        wave_sync();
+        for (int32_t base = j0; base < j1; base += 64 * DPL) {
+            // Every answer of every shape is reached by a projection, so a
+            // candidate without an in-edge is a non-answer: the in-edge mask
+            // (V bits, resident in the last-level cache) decides most draws
+            // without touching the adjacency.
+            int32_t c[DPL];
+            uint32_t bit[DPL];
+#pragma unroll
+            for (int k = 0; k < DPL; ++k) {
+                const int32_t j = base + k * 64 + lane;
+                c[k] = 0;
+                bit[k] = 0;
+                if (j < j1) {
+                    c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
+                    bit[k] = g.has_in[c[k] >> 5];
+                }
+            }
+            int32_t n0[DPL], n1[DPL];
+#pragma unroll
+            for (int k = 0; k < DPL; ++k) {
+                bit[k] = (bit[k] >> (c[k] & 31)) & 1u;
+                n0[k] = n1[k] = 0;
+                if (bit[k]) {
+                    n0[k] = g.rev.node[c[k]];
+                    n1[k] = g.rev.node[c[k] + 1];
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < DPL; ++k) {
+                const int32_t j = base + k * 64 + lane;
+                if (j >= j1) continue;
+                tl.read(g.has_in + (c[k] >> 5), 4);
+                int32_t st = ST_NON;
+                if (bit[k]) {
+                    tl.read(g.rev.node + c[k], 8);
+                    st = cand_test<QT>(g, F, anc, rel, c[k], n0[k], n1[k], tl);
+                }
+                const int64_t at = (int64_t)b * p.neg_tries + j;
+                ws.cval[at] = c[k];
+                ws.status[at] = (uint8_t)st;
+                if (st == ST_PEND) {
+                    const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers every draw of a round
+                    ws.queue[slot] = make_int2(b, j);
+                }
             }
         }
         flush_tally(tl, stats, b, lane);
-        __syncthreads();   // the next item restages the lists
+        wave_sync();   // the next query restages the wave's slice
     }
 }
 
@@ -608,15 +693,12 @@ __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p,
                                                     Ws ws, int64_t* stats)
 {
     const int lane = threadIdx.x & 63;
-    const int32_t total = uni(__atomic_load_n(&ws.ctrl[0], __ATOMIC_RELAXED));
+    const int32_t total = uni(ws.ctrl[0]);
+    const int32_t nwaves = gridDim.x * (HEAVY_WG / 64);
     T tl;
-    // every pass pops one item or leaves, so total + 1 passes always suffice;
-    // the popped index is made wave-uniform so the wave stays converged
-    for (int32_t pass = 0; pass <= total; ++pass) {
-        int32_t idx = 0;
-        if (lane == 0) idx = atomicAdd(&ws.ctrl[1], 1);
-        idx = uni(__shfl(idx, 0));
-        if (idx >= total) break;
+    // wavefront w takes items w, w + nwaves, ... (no shared counter to contend on)
+    for (int32_t idx = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6)); idx < total;
+         idx += nwaves) {
         const int2 it = ws.queue[idx];
         const int32_t b = uni(it.x), j = uni(it.y);
         const int64_t at = (int64_t)b * p.neg_tries + j;
@@ -803,6 +885,7 @@ GraphView view_of(const smore_graph* g)
     gv.fwd = DirView{g->f_node, g->f_grp, g->f_nbr};
     gv.rev = DirView{g->r_node, g->r_grp, g->r_nbr};
     gv.active_in = g->active_in;
+    gv.has_in = g->has_in;
     gv.V = g->V;
     gv.n_active = (int32_t)g->n_active;
     return gv;

@@ -23,6 +23,7 @@ struct DirView {
 struct GraphView {
     DirView fwd, rev;
     const int32_t* active_in;  // entities with an in-edge, ascending
+    const uint32_t* has_in;    // bit v: entity v has an in-edge (V bits, cache-resident)
     int32_t V;
     int32_t n_active;
 };
@@ -60,6 +61,7 @@ struct smore_graph {
     int64_t E, S_fwd, S_rev, n_active;
     int32_t *f_node, *f_nbr, *r_node, *r_nbr, *active_in;
     int2 *f_grp, *r_grp;
+    uint32_t* has_in;
     size_t bytes;
 };
 

@@ -41,6 +41,9 @@ def check_graph(g, og):
         oe, orl, onb = og.dump(reverse=bool(d))
         assert np.array_equal(ent, oe) and np.array_equal(rel, orl) and np.array_equal(nb, onb), d
     assert np.array_equal(g.copy(6, og.n_active), og.active_in())
+    words = g.copy(7, (g.V + 31) // 32).view(np.uint32)
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little")[:g.V]
+    assert np.array_equal(np.nonzero(bits)[0], og.active_in())
 
 
 @pytest.mark.parametrize("case", ["dups", "dups_inverse", "tiny", "fb15k237", "fb400k", "empty",
