@@ -21,15 +21,14 @@ __device__ __forceinline__ U4 philox4x32_10(U4 c, uint32_t k0, uint32_t k1)
 {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint32_t lo_a = 0xD2511F53u * c.x;
-        const uint32_t hi_a = __umulhi(0xD2511F53u, c.x);
-        const uint32_t lo_b = 0xCD9E8D57u * c.z;
-        const uint32_t hi_b = __umulhi(0xCD9E8D57u, c.z);
+        // one 32x32->64 product per multiplier (a single v_mad_u64_u32)
+        const uint64_t pa = (uint64_t)0xD2511F53u * c.x;
+        const uint64_t pb = (uint64_t)0xCD9E8D57u * c.z;
         U4 n;
-        n.x = hi_b ^ c.y ^ k0;
-        n.y = lo_b;
-        n.z = hi_a ^ c.w ^ k1;
-        n.w = lo_a;
+        n.x = (uint32_t)(pb >> 32) ^ c.y ^ k0;
+        n.y = (uint32_t)pb;
+        n.z = (uint32_t)(pa >> 32) ^ c.w ^ k1;
+        n.w = (uint32_t)pa;
         c = n;
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;

@@ -587,11 +587,14 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
 }
 
 // One wavefront per active query (persistent over the list, several
-// queries per workgroup and no workgroup barrier): the query's lists are
-// staged once into the wave's LDS slice, then each lane takes DPL draws of
-// the round at a time, issuing all their first loads before deciding them
-// one by one.
-constexpr int DPL = 4;
+// queries per workgroup and no workgroup barrier).  The query's lists are
+// staged once into the wave's LDS slice.  Draws are taken WIN at a time:
+// every lane computes WIN / 64 draws and reads their in-edge bits (all
+// loads in flight together); the draws with an in-edge are compacted into
+// the wave's survivor list and then verified one per lane, so a window
+// costs one dependent chain per 64 survivors instead of one per draw slot.
+constexpr int WIN = 512;
+constexpr int DPW = WIN / 64;
 
 __device__ __forceinline__ void wave_sync()
 {
@@ -606,8 +609,13 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                                                     int32_t j1)
 {
     __shared__ int32_t stage_all[CWG / 64][STAGE];
+    __shared__ int32_t sc_all[CWG / 64][WIN];
+    __shared__ int32_t sj_all[CWG / 64][WIN];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     int32_t* stage = stage_all[w];
+    int32_t* sc = sc_all[w];
+    int32_t* sj = sj_all[w];
+    const uint64_t below = lanes_below(lane);
     const int32_t nact = uni(ws.ctrl[2 + cur]);
     const int32_t nwaves = gridDim.x * (CWG / 64);
     T tl;
@@ -635,52 +643,58 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 F[f] = FSet{g.fwd.nbr + beg, n, false};
             }
         }
-        wave_sync();
-        for (int32_t base = j0; base < j1; base += 64 * DPL) {
+        int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
+        uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
+        for (int32_t base = j0; base < j1; base += WIN) {
             // Every answer of every shape is reached by a projection, so a
-            // candidate without an in-edge is a non-answer: the in-edge mask
-            // (V bits, resident in the last-level cache) decides most draws
-            // without touching the adjacency.
-            int32_t c[DPL];
-            uint32_t bit[DPL];
+            // draw without an in-edge is a non-answer: the in-edge mask (V
+            // bits, resident in the last-level cache) decides most draws.
+            int32_t c[DPW];
+            uint32_t word[DPW];
 #pragma unroll
-            for (int k = 0; k < DPL; ++k) {
+            for (int k = 0; k < DPW; ++k) {
                 const int32_t j = base + k * 64 + lane;
                 c[k] = 0;
-                bit[k] = 0;
+                word[k] = 0;
                 if (j < j1) {
                     c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
-                    bit[k] = g.has_in[c[k] >> 5];
+                    word[k] = g.has_in[c[k] >> 5];
                 }
             }
-            int32_t n0[DPL], n1[DPL];
+            int32_t nsurv = 0;
 #pragma unroll
-            for (int k = 0; k < DPL; ++k) {
-                bit[k] = (bit[k] >> (c[k] & 31)) & 1u;
-                n0[k] = n1[k] = 0;
-                if (bit[k]) {
-                    n0[k] = g.rev.node[c[k]];
-                    n1[k] = g.rev.node[c[k] + 1];
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < DPL; ++k) {
+            for (int k = 0; k < DPW; ++k) {
                 const int32_t j = base + k * 64 + lane;
-                if (j >= j1) continue;
-                tl.read(g.has_in + (c[k] >> 5), 4);
-                int32_t st = ST_NON;
-                if (bit[k]) {
-                    tl.read(g.rev.node + c[k], 8);
-                    st = cand_test<QT>(g, F, anc, rel, c[k], n0[k], n1[k], tl);
+                const bool live = j < j1;
+                const bool in = live && ((word[k] >> (c[k] & 31)) & 1u);
+                if (live) {
+                    tl.read(g.has_in + (c[k] >> 5), 4);
+                    cv[j] = c[k];
+                    if (!in) sv[j] = ST_NON;
                 }
-                const int64_t at = (int64_t)b * p.neg_tries + j;
-                ws.cval[at] = c[k];
-                ws.status[at] = (uint8_t)st;
-                if (st == ST_PEND) {
-                    const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers every draw of a round
-                    ws.queue[slot] = make_int2(b, j);
+                const uint64_t m = __ballot(in);
+                if (in) {
+                    const int32_t at = nsurv + __popcll(m & below);
+                    sc[at] = c[k];
+                    sj[at] = j;
+                }
+                nsurv += __popcll(m);
+            }
+            wave_sync();
+            for (int32_t s0 = 0; s0 < nsurv; s0 += 64) {
+                if (s0 + lane < nsurv) {
+                    const int32_t cc = sc[s0 + lane], j = sj[s0 + lane];
+                    const int32_t n0 = g.rev.node[cc], n1 = g.rev.node[cc + 1];
+                    tl.read(g.rev.node + cc, 8);
+                    const int32_t st = cand_test<QT>(g, F, anc, rel, cc, n0, n1, tl);
+                    sv[j] = (uint8_t)st;
+                    if (st == ST_PEND) {
+                        const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers a round
+                        ws.queue[slot] = make_int2(b, j);
+                    }
                 }
             }
+            wave_sync();   // the next window reuses the survivor list
         }
         flush_tally(tl, stats, b, lane);
         wave_sync();   // the next query restages the wave's slice
