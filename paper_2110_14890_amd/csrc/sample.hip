@@ -160,6 +160,39 @@ __device__ __forceinline__ void search4(const int32_t* B, int32_t nb, const int3
     }
 }
 
+// search4 with a target list per key (lists of different lengths; the loop
+// runs until every key of the lane is settled).
+template <class T>
+__device__ __forceinline__ void search4v(const int32_t* const* B, const int32_t* nb, const int32_t* x,
+                                         const bool* count, bool* found, T& tl)
+{
+    int32_t base[4] = {0, 0, 0, 0}, n[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) n[k] = nb[k];
+    for (;;) {
+        bool more = false;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (n[k] > 1) {
+                const int32_t half = n[k] >> 1;
+                if (count[k]) tl.read(B[k] + base[k] + half, 4);
+                base[k] = B[k][base[k] + half] <= x[k] ? base[k] + half : base[k];
+                n[k] -= half;
+                more |= n[k] > 1;
+            }
+        }
+        if (!more) break;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        found[k] = false;
+        if (nb[k] > 0) {
+            if (count[k]) tl.read(B[k] + base[k], 4);
+            found[k] = B[k][base[k]] == x[k];
+        }
+    }
+}
+
 // Does some element of K[0..nk) occur in L[0..nl)?  Whole wavefront, 256
 // keys per step (four per lane).  k_glob / l_glob: whether reads of the
 // list count as graph traffic.
@@ -354,13 +387,13 @@ struct Ws {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Round r covers draws [bound(r-1), bound(r)): first n_neg plus a margin,
-// then doubling, up to neg_tries.
+// Round r covers draws [round_end(r-1), round_end(r)): first n_neg plus a
+// margin, then four times as many, up to neg_tries.
 inline int32_t round_end(const SampleParams& p, int r)
 {
     int64_t e = p.n_neg + p.n_neg / 16 + 32;
     e = (e + 63) / 64 * 64;
-    for (int k = 0; k < r; ++k) e *= 2;
+    for (int k = 0; k < r; ++k) e *= 4;
     return (int32_t)(e < p.neg_tries ? e : p.neg_tries);
 }
 
@@ -512,16 +545,65 @@ __device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel
         return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl) ||
                wave_meet(S, ns, true, F[1].p, F[1].n, false, lane, tl);
     if (QT == Q3P) {
+        // second backward step for 64 entities y of R_r2(c) at a time; every
+        // pair (y, key) with key from the shorter of R_r1(y) and F0 is one
+        // search in the longer, and all pairs of the 64 y's are spread over
+        // the wavefront, four per lane, so they share one search chain
         for (int32_t k = 0; k < ns; k += 64) {
             if (lane == 0) tl.read(S + k, 4 * min(64, ns - k));
             int2 s2 = make_int2(0, 0);
             if (k + lane < ns) s2 = group_range(g.rev, S[k + lane], rel[1], tl);
-            uint64_t todo = __ballot(s2.y > s2.x);
-            while (todo) {
-                const int src = __ffsll((unsigned long long)todo) - 1;
-                todo &= todo - 1;
-                const int32_t x = uni(__shfl(s2.x, src)), y = uni(__shfl(s2.y, src));
-                if (wave_meet(g.rev.nbr + x, y - x, true, F[0].p, F[0].n, false, lane, tl)) return true;
+            const int32_t len = s2.y - s2.x;
+            const bool keys_in_list = len <= F[0].n;       // search R_r1(y) entries in F0
+            const int32_t npair = len > 0 ? min(len, F[0].n) : 0;
+            int32_t incl = npair;                           // inclusive prefix over the lanes
+            for (int d = 1; d < 64; d <<= 1) {
+                const int32_t v = __shfl_up(incl, d);
+                if (lane >= d) incl += v;
+            }
+            const int32_t total = uni(__shfl(incl, 63));
+            const int32_t excl = incl - npair;
+            for (int32_t p0 = 0; p0 < total; p0 += 256) {
+                const int32_t* Bk[4];
+                int32_t nbk[4], x[4];
+                bool cnt[4], found[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int32_t pi = p0 + 64 * u + lane;
+                    const int32_t pq = pi < total ? pi : total - 1;
+                    // owner lane of pair pq: the highest lane whose exclusive
+                    // prefix is <= pq (binary lifting, every lane active)
+                    int32_t lo = 0;
+#pragma unroll
+                    for (int step = 32; step >= 1; step >>= 1) {
+                        const int32_t cand = lo + step;
+                        const int32_t ev = __shfl(excl, cand > 63 ? 63 : cand);
+                        if (cand <= 63 && ev <= pq) lo = cand;
+                    }
+                    const int32_t off = pq - __shfl(excl, lo);
+                    const int32_t lx = __shfl(s2.x, lo);
+                    const int32_t ln = __shfl(len, lo);
+                    const int32_t kil = __shfl((int32_t)keys_in_list, lo);
+                    Bk[u] = F[0].p;
+                    nbk[u] = 0;
+                    x[u] = -1;
+                    cnt[u] = false;
+                    if (pi < total) {
+                        if (kil) {
+                            x[u] = g.rev.nbr[lx + off];
+                            tl.read(g.rev.nbr + lx + off, 4);
+                            Bk[u] = F[0].p;
+                            nbk[u] = F[0].n;
+                        } else {
+                            x[u] = F[0].p[off];
+                            Bk[u] = g.rev.nbr + lx;
+                            nbk[u] = ln;
+                            cnt[u] = true;
+                        }
+                    }
+                }
+                search4v(Bk, nbk, x, cnt, found, tl);
+                if (__ballot(found[0] || found[1] || found[2] || found[3])) return true;
             }
         }
         return false;
@@ -704,9 +786,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
 // Persistent wavefronts draining the heavy queue.
 template <int QT, class T>
 __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p, smore_sample_out out,
-                                                    Ws ws, int64_t* stats)
+                                                    Ws ws, int64_t* stats, int nxt)
 {
     const int lane = threadIdx.x & 63;
+    // the compaction that follows appends to the next round's list
+    if (blockIdx.x == 0 && threadIdx.x == 0) ws.ctrl[2 + nxt] = 0;
     const int32_t total = uni(ws.ctrl[0]);
     const int32_t nwaves = gridDim.x * (HEAVY_WG / 64);
     T tl;
@@ -754,78 +838,85 @@ __device__ __forceinline__ int32_t ht_first(const int32_t* tv, const int32_t* tj
     return tj[h];
 }
 
-// Per active query: keep draw j iff it is not an answer and no earlier draw
-// has the same value; the first n_neg kept, in draw order, are the
-// negatives.  Queries that are neither complete nor out of budget go to the
-// next round's list.
-__global__ __launch_bounds__(CWG) void k_compact(SampleParams p, smore_sample_out out, Ws ws, int cur,
-                                                 int32_t j_end, int last, int32_t tcap, int tshift)
+// Per active query, one wavefront per query (one-wave workgroups; the LDS
+// holds the round's first-occurrence table and the query's draws and
+// states): keep draw j iff it is not an answer and no earlier draw has the
+// same value; the first n_neg kept, in draw order, are the negatives.
+// Queries neither complete nor out of budget go to the next round's list.
+__global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out out, Ws ws, int cur,
+                                                int32_t j_end, int last, int32_t tcap, int tshift)
 {
     extern __shared__ int32_t lds[];
     int32_t* tv = lds;
     int32_t* tj = lds + tcap;
-    __shared__ int32_t s_cnt[CWG / 64];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    int32_t* vals = lds + 2 * tcap;
+    uint8_t* sts = (uint8_t*)(vals + j_end);
+    const int lane = threadIdx.x;
+    const uint64_t below = lanes_below(lane);
     const uint32_t tmask = (uint32_t)tcap - 1;
     const int32_t nact = uni(ws.ctrl[2 + cur]);
+    // the heavy queue of this round is drained: ready it for the next round
+    if (blockIdx.x == 0 && lane == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
     for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
         const int32_t b = uni(ws.act[cur][qi]);
         const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
-        for (int32_t k = tid; k < tcap; k += CWG) { tv[k] = -1; tj[k] = INT_MAX; }
-        __syncthreads();
-        for (int32_t j = tid; j < j_end; j += CWG) ht_insert(tv, tj, tmask, tshift, cv[j], j);
-        __syncthreads();
+        for (int32_t k = lane; k < tcap; k += 64) { tv[k] = -1; tj[k] = INT_MAX; }
+        for (int32_t j = lane; j < j_end; j += 64) {
+            vals[j] = cv[j];
+            sts[j] = sv[j];
+        }
+        wave_sync();
+        for (int32_t j = lane; j < j_end; j += 64) ht_insert(tv, tj, tmask, tshift, vals[j], j);
+        wave_sync();
         int32_t acc = 0;
-        for (int32_t row0 = 0; row0 < j_end && acc < p.n_neg; row0 += CWG) {
-            const int32_t j = row0 + tid;
+        for (int32_t row0 = 0; row0 < j_end && acc < p.n_neg; row0 += 64) {
+            const int32_t j = row0 + lane;
             int32_t c = 0;
             bool keep = false;
             if (j < j_end) {
-                c = cv[j];
-                keep = sv[j] == ST_NON && ht_first(tv, tj, tmask, tshift, c) == j;
+                c = vals[j];
+                keep = sts[j] == ST_NON && ht_first(tv, tj, tmask, tshift, c) == j;
             }
             const uint64_t m = __ballot(keep);
-            if (lane == 0) s_cnt[w] = __popcll(m);
-            __syncthreads();
-            int32_t before = acc, total = 0;
-            for (int ww = 0; ww < CWG / 64; ++ww) {
-                if (ww < w) before += s_cnt[ww];
-                total += s_cnt[ww];
-            }
-            const int32_t rank = before + __popcll(m & lanes_below(lane));
+            const int32_t rank = acc + __popcll(m & below);
             if (keep && rank < p.n_neg) {
                 row[rank] = c;
                 if (rank == p.n_neg - 1) out.neg_draws[b] = j + 1;
             }
-            acc = uni(min(p.n_neg, acc + total));
-            __syncthreads();
+            acc = uni(min(p.n_neg, acc + __popcll(m)));
         }
         if (acc == p.n_neg || last) {
-            for (int32_t k = acc + tid; k < p.n_neg; k += CWG) row[k] = -1;
-            if (tid == 0) {
+            for (int32_t k = acc + lane; k < p.n_neg; k += 64) row[k] = -1;
+            if (lane == 0) {
                 out.n_valid[b] = acc;
                 if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
             }
-        } else if (tid == 0) {
+        } else if (lane == 0) {
             ws.act[cur ^ 1][atomicAdd(&ws.ctrl[2 + (cur ^ 1)], 1)] = b;
         }
-        __syncthreads();
+        wave_sync();
     }
-}
-
-// Resets the queue counters and the next round's list size.
-__global__ void k_round_begin(Ws ws, int nxt)
-{
-    ws.ctrl[0] = 0;
-    ws.ctrl[1] = 0;
-    ws.ctrl[2 + nxt] = 0;
 }
 
 __global__ void k_init(Ws ws)
 {
     for (int k = threadIdx.x; k < 64; k += blockDim.x) ws.ctrl[k] = 0;
+}
+
+// first-occurrence table of the compaction: load factor at most 0.6
+inline int32_t compact_tcap(int32_t j_end)
+{
+    int32_t tcap = 64;
+    while (tcap * 3 < 5 * j_end) tcap <<= 1;
+    return tcap;
+}
+
+// table (value, first draw) + the query's draws and states
+inline size_t compact_lds(int32_t j_end)
+{
+    return (size_t)2 * compact_tcap(j_end) * sizeof(int32_t) + (size_t)j_end * 5 + 16;
 }
 
 inline int check_launch(const char** err)
@@ -849,26 +940,24 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
         const int32_t j_end = round_end(p, r);
-        k_round_begin<<<1, 1, 0, st>>>(ws, cur ^ 1);
         k_candidates<QT, T><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
         if ((rc = check_launch(err))) return rc;
-        k_heavy<QT, T><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats);
+        k_heavy<QT, T><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
-        int32_t tcap = 64;
-        while (tcap < 2 * j_end) tcap <<= 1;
+        const int32_t tcap = compact_tcap(j_end);
         int tshift = 32;
         for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
-        const size_t lds = (size_t)2 * tcap * sizeof(int32_t);
+        const size_t lds = compact_lds(j_end);
         static bool attr = false;
         if (lds > 65536 && !attr) {
             const hipError_t e = hipFuncSetAttribute((const void*)k_compact,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                     (int)(4 * 2 * SMORE_MAX_NEG_TRIES * sizeof(int32_t)));
+                                                     (int)compact_lds(SMORE_MAX_NEG_TRIES));
             if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
             attr = true;
         }
-        k_compact<<<PERSIST_BLOCKS, CWG, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
-                                                    tshift);
+        k_compact<<<PERSIST_BLOCKS * 4, 64, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
+                                                       tshift);
         if ((rc = check_launch(err))) return rc;
         prev = j_end;
     }
