@@ -39,6 +39,23 @@ def workload_name(cfg):
             f"{'/'.join(cfg.query_types)} batch {cfg.batch:,}, {cfg.n_neg} negatives")
 
 
+def traffic_for(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE scaled by the copy calibration, plus WRITE_SIZE),
+    or None when the summary was taken on other kernel sources."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "counters_freebase.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        prof = json.load(f)
+    src = os.path.join(ROOT, "paper_2110_14890_amd", "csrc", "sample.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if prof.get("sample_hip_sha256_16") != sha or kernel not in prof.get("kernels", {}):
+        return None
+    return prof["kernels"][kernel]["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(cfg, triples, types, seconds, threads):
     """The CPU oracle, timed on the host on the first queries of each shape
     (a bounded sample of the same workload)."""
@@ -131,16 +148,18 @@ def main():
     argv = {qt: sm.make_args(cfg.batch, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries) for qt in types}
     outs = {qt: sm.alloc_outputs(cfg.batch, cfg.n_neg) for qt in types}
 
-    # untimed accounting pass: graph bytes / 64-byte lines each verification reads
+    # untimed accounting pass: graph bytes / 64-byte lines the verification
+    # reads, [0:2] in the candidate kernel, [2:4] in the long-list kernel
     acct = {}
     for qt in types:
-        stats = torch.zeros((cfg.batch, 2), dtype=torch.int64, device="cuda")
+        stats = torch.zeros((cfg.batch, 4), dtype=torch.int64, device="cuda")
         sm.sample_positives(g, dags[qt], argv[qt], outs[qt], stream)
         sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], stats, stream)
         torch.cuda.synchronize()
         st = stats.sum(0).cpu().numpy()
         nv = outs[qt]["n_valid"].cpu().numpy()
-        acct[qt] = {"bytes": int(st[0]), "lines": int(st[1]),
+        acct[qt] = {"cand_bytes": int(st[0]), "cand_lines": int(st[1]),
+                    "heavy_bytes": int(st[2]), "heavy_lines": int(st[3]),
                     "valid": int((nv >= 0).sum()), "complete": int((nv == cfg.n_neg).sum()),
                     "draws": int(outs[qt]["neg_draws"].clamp(min=0).sum().item())}
         log(f"{qt}: {acct[qt]}")
@@ -152,6 +171,7 @@ def main():
             sm.sample_positives(g, dags[qt], argv[qt], outs[qt], stream)
             if ev is not None:
                 ev[qt][1].record(stream)
+                sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
             sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, stream)
             if ev is not None:
                 ev[qt][2].record(stream)
@@ -159,8 +179,13 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(3)] for qt in types}
+    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for qt in types}
            for _ in range(args.steps)]
+    for e in evs:                       # create the HIP events before the timed region
+        for qt in types:
+            for x in e[qt]:
+                x.record(stream)
+    torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -173,38 +198,42 @@ def main():
     ms_step = ms_total / args.steps
     per_type = {}
     for qt in types:
-        pos = np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs])
-        neg = np.mean([e[qt][1].elapsed_time(e[qt][2]) for e in evs])
+        pos = float(np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs]))
+        neg = float(np.mean([e[qt][1].elapsed_time(e[qt][2]) for e in evs]))
+        cand = float(np.mean([e[qt][3].elapsed_time(e[qt][4]) for e in evs]))
         a = acct[qt]
         per_type[qt] = {
             "queries_per_s": cfg.batch / ((pos + neg) / 1e3),
             "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3),
-            "positive_ms": pos, "verify_ms": neg,
-            "verify_line_GBps": a["lines"] * 64 / (neg / 1e3) / 1e9,
-            "verify_useful_GBps": a["bytes"] / (neg / 1e3) / 1e9,
+            "positive_ms": pos, "negative_stage_ms": neg, "candidate_kernel_ms": cand,
+            "candidate_kernel_line_GBps": a["cand_lines"] * 64 / (cand / 1e3) / 1e9,
+            "candidate_kernel_useful_GBps": a["cand_bytes"] / (cand / 1e3) / 1e9,
             "draws_per_query": a["draws"] / max(a["valid"], 1),
-            "line_bytes_per_query": a["lines"] * 64 / max(a["valid"], 1),
-            "useful_bytes_per_query": a["bytes"] / max(a["valid"], 1),
+            "cand_line_bytes_per_query": a["cand_lines"] * 64 / max(a["valid"], 1),
+            "cand_useful_bytes_per_query": a["cand_bytes"] / max(a["valid"], 1),
+            "heavy_useful_bytes_per_query": a["heavy_bytes"] / max(a["valid"], 1),
             "valid": a["valid"], "complete": a["complete"],
         }
         log(f"{qt}: {per_type[qt]}")
     value = cfg.batch * len(types) / (ms_step / 1e3)
 
-    # dominant kernel: the verification kernel with the largest time
-    dom = max(types, key=lambda qt: per_type[qt]["verify_ms"])
+    # dominant kernel: the candidate kernel (the largest single kernel of the
+    # step) of the shape where it takes longest; timed by events the library
+    # records around it on the sampling stream
+    dom = max(types, key=lambda qt: per_type[qt]["candidate_kernel_ms"])
     d = per_type[dom]
-    achieved = d["verify_useful_GBps"]
+    achieved = d["candidate_kernel_line_GBps"]
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 5), "traffic": None,
-                "kernel": f"negative sampling of {dom} (smore_sample_negatives)",
-                "bytes_per_launch": acct[dom]["bytes"],
-                "bytes_per_query": round(acct[dom]["bytes"] / max(acct[dom]["valid"], 1), 1),
-                "avg_launch_ms": round(d["verify_ms"], 4),
-                "accounting": "graph bytes the verification reads per query: forward-cached "
-                              "lists once, then per candidate draw its reverse node pointers, "
-                              "relation-search probes, group bounds and backward lists (and the "
-                              "searches into long lists); lookups inside forward-cached lists "
-                              "are not counted"}
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 5),
+                "traffic": traffic_for(f"k_candidates<{dom}>"),
+                "kernel": f"k_candidates<{dom}> (first round of smore_sample_negatives)",
+                "bytes_per_launch": acct[dom]["cand_lines"] * 64,
+                "useful_bytes_per_launch": acct[dom]["cand_bytes"],
+                "avg_launch_ms": round(d["candidate_kernel_ms"], 4),
+                "accounting": "64-byte lines of graph data per dependent read of the candidate "
+                              "kernel (in-edge mask word, reverse node pointers, relation-search "
+                              "probes, group bounds, short backward lists, forward lists staged "
+                              "once per query), times 64, summed over the launch"}
 
     cpu = None
     if not args.no_cpu_baseline:

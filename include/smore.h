@@ -173,19 +173,30 @@ int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_s
    positive < 0, or with an anchor or relation id used by the shape outside
    the graph's range, is skipped: negatives -1, n_valid -1, neg_draws -1) and
    writes negatives, n_valid and neg_draws; it may be run on queries built
-   by the caller.  stats is NULL or a device int64 [batch, 2] array that
+   by the caller.  stats is NULL or a device int64 [batch, 4] array that
    receives, per query, the bytes and the 64-byte lines of graph data the
-   verification read (forward-cached lists once per query, every read made
-   from a candidate's side; lookups inside forward-cached lists are cache
-   hits of the method and are not counted); counting makes the call slower
-   and does not change any other output.  workspace / ws_bytes as for
-   smore_sample (smore_sample_positives needs none). */
+   verification read: [0], [1] in the candidate kernel (forward-cached lists
+   once per query, then every read made from a candidate's side), [2], [3]
+   in the kernel that intersects long lists; lookups inside forward-cached
+   lists are cache hits of the method and are not counted.  Counting makes
+   the call slower and does not change any other output.  workspace /
+   ws_bytes as for smore_sample (smore_sample_positives needs none). */
 int smore_sample_positives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
                            void *hip_stream);
 int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
                            int64_t *stats, void *workspace, size_t ws_bytes, void *hip_stream);
+
+/* Instrumentation: the next smore_sample or smore_sample_negatives call
+   made by this thread records the caller's HIP events (hipEvent_t) on its
+   stream immediately before and after one of its kernels in the first
+   round of candidate draws: which = 0 the candidate kernel, 1 the kernel
+   that intersects long lists, 2 the ordered selection.  One-shot: the
+   next call that reaches its kernel launches disarms it whether or not it
+   recorded.  Either event NULL disarms.  The events stay owned by the
+   caller.  Returns SMORE_E_INVALID_ARG for another `which`. */
+int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
 
 /* Release a graph (NULL is a no-op). */
 void smore_free_graph(smore_graph *g);

@@ -83,6 +83,7 @@ def lib() -> ctypes.CDLL:
         L.smore_sample_negatives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp, c_vp, ctypes.c_size_t, c_vp]
+        L.smore_profile_kernel.argtypes = [c_vp, c_vp, c_i32]
         L.smore_free_graph.argtypes = [c_vp]
         L.smore_free_graph.restype = None
         _lib = L
@@ -238,14 +239,28 @@ def sample_positives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, s
 def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stats=None,
                      stream=None, workspace: "Workspace | None" = None) -> dict:
     """Second stage only (smore_sample_negatives) on the queries in `out`;
-    stats: optional int64 [batch, 2] device tensor of (bytes, 64-byte lines)
-    of graph data read per query."""
+    stats: optional int64 [batch, 4] device tensor: (bytes, 64-byte lines) of
+    graph data read per query by the candidate kernel, then by the kernel
+    that intersects long lists."""
     sp = c_vp(stats.data_ptr()) if stats is not None else None
     wp, wn = _workspace(workspace, dag, args)
     _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                                         ctypes.byref(_out_struct(out)), sp, wp, wn,
                                         _stream_handle(stream)))
     return out
+
+
+KERNEL_CANDIDATES, KERNEL_HEAVY, KERNEL_SELECT = 0, 1, 2
+
+
+def profile_kernel(start_event, stop_event, which: int = KERNEL_CANDIDATES) -> None:
+    """Arm torch.cuda.Event objects (enable_timing=True) to be recorded around
+    one kernel of the next negatives call on this thread (smore_profile_kernel)."""
+    for ev in (start_event, stop_event):
+        if not ev.cuda_event:          # torch creates the HIP event on first use
+            ev.record()
+    _check(lib().smore_profile_kernel(c_vp(start_event.cuda_event), c_vp(stop_event.cuda_event),
+                                      which))
 
 
 def sample(graph: Graph, qtype: "str | QueryDag", batch: int, n_neg: int, seed: int = 0,

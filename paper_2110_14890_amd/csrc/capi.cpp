@@ -330,6 +330,13 @@ int smore_graph_copy(const smore_graph* g, int32_t which, int32_t* host_dst, int
     return ok();
 }
 
+int smore_profile_kernel(void* start_event, void* stop_event, int32_t which)
+{
+    if (which < 0 || which > 2) return fail(SMORE_E_INVALID_ARG, "which must be 0, 1 or 2");
+    smore::arm_profile(start_event, stop_event, which);
+    return ok();
+}
+
 void smore_free_graph(smore_graph* g)
 {
     if (!g) return;

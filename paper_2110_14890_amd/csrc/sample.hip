@@ -440,7 +440,7 @@ size_t ws_layout(const SampleParams& p, Ws* w, char* base)
 // Tally of one lane summed over its wavefront and added to the query's
 // counters (the wavefront must be converged).
 template <class T>
-__device__ __forceinline__ void flush_tally(T& tl, int64_t* stats, int32_t b, int lane)
+__device__ __forceinline__ void flush_tally(T& tl, int64_t* stats, int32_t b, int lane, int slot = 0)
 {
     if constexpr (T::on) {
         uint64_t x = tl.b, y = tl.l;
@@ -449,8 +449,8 @@ __device__ __forceinline__ void flush_tally(T& tl, int64_t* stats, int32_t b, in
             y += __shfl_xor(y, s);
         }
         if (lane == 0 && (x | y)) {
-            atomicAdd((unsigned long long*)&stats[2 * (int64_t)b], (unsigned long long)x);
-            atomicAdd((unsigned long long*)&stats[2 * (int64_t)b + 1], (unsigned long long)y);
+            atomicAdd((unsigned long long*)&stats[4 * (int64_t)b + slot], (unsigned long long)x);
+            atomicAdd((unsigned long long*)&stats[4 * (int64_t)b + slot + 1], (unsigned long long)y);
         }
         tl.b = tl.l = 0;
     }
@@ -633,7 +633,8 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     if (b >= p.batch) return;
     int32_t anc[3], rel[3];
     int32_t* row = out.negatives + (int64_t)b * p.n_neg;
-    if (stats) { stats[2 * (int64_t)b] = 0; stats[2 * (int64_t)b + 1] = 0; }
+    if (stats)
+        for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
     if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
         for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
         out.n_valid[b] = -1;
@@ -663,8 +664,8 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     q[6] = staged;
     ws.act[0][atomicAdd(&ws.ctrl[2], 1)] = b;
     if constexpr (T::on) {
-        stats[2 * (int64_t)b] = (int64_t)tl.b;
-        stats[2 * (int64_t)b + 1] = (int64_t)tl.l;
+        stats[4 * (int64_t)b] = (int64_t)tl.b;
+        stats[4 * (int64_t)b + 1] = (int64_t)tl.l;
     }
 }
 
@@ -812,7 +813,7 @@ __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p,
         }
         const bool ans = heavy_test<QT>(g, F, rel, c, lane, tl);
         if (lane == 0) ws.status[at] = ans ? ST_ANS : ST_NON;
-        flush_tally(tl, stats, b, lane);
+        flush_tally(tl, stats, b, lane, 2);
     }
 }
 
@@ -926,6 +927,19 @@ inline int check_launch(const char** err)
     return SMORE_OK;
 }
 
+struct ProfileArm {
+    hipEvent_t start = nullptr, stop = nullptr;
+    int which = -1;
+};
+thread_local ProfileArm g_prof;
+
+inline void prof_mark(int which, int round, bool after, hipStream_t st)
+{
+    if (round != 0 || g_prof.which != which || !g_prof.start || !g_prof.stop) return;
+    (void)hipEventRecord(after ? g_prof.stop : g_prof.start, st);
+    if (after) g_prof = ProfileArm{};
+}
+
 template <int QT, class T>
 int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample_out& out, Ws ws,
                   int64_t* stats, int32_t R, hipStream_t st, const char** err)
@@ -940,10 +954,14 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
         const int32_t j_end = round_end(p, r);
+        prof_mark(0, r, false, st);
         k_candidates<QT, T><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
         if ((rc = check_launch(err))) return rc;
+        prof_mark(0, r, true, st);
+        prof_mark(1, r, false, st);
         k_heavy<QT, T><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
+        prof_mark(1, r, true, st);
         const int32_t tcap = compact_tcap(j_end);
         int tshift = 32;
         for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
@@ -956,9 +974,11 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
             attr = true;
         }
+        prof_mark(2, r, false, st);
         k_compact<<<PERSIST_BLOCKS * 4, 64, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
                                                        tshift);
         if ((rc = check_launch(err))) return rc;
+        prof_mark(2, r, true, st);
         prev = j_end;
     }
     return SMORE_OK;
@@ -996,6 +1016,13 @@ GraphView view_of(const smore_graph* g)
 
 }  // namespace
 
+void arm_profile(void* start_event, void* stop_event, int which)
+{
+    g_prof.start = (hipEvent_t)start_event;
+    g_prof.stop = (hipEvent_t)stop_event;
+    g_prof.which = (start_event && stop_event) ? which : -1;
+}
+
 size_t negatives_workspace_bytes(const SampleParams& p)
 {
     return ws_layout(p, nullptr, nullptr);
@@ -1019,8 +1046,10 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
         return SMORE_E_INVALID_ARG;
     }
     const GraphView gv = view_of(g);
-    if (stats) return dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, st, err);
-    return dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
+    const int rc = stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, st, err)
+                         : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
+    g_prof = ProfileArm{};  // one-shot: an arm never outlives the call it was meant for
+    return rc;
 }
 
 }  // namespace smore

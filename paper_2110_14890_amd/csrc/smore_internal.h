@@ -75,4 +75,6 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
                     const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
                     hipStream_t stream, const char** err);
 size_t negatives_workspace_bytes(const SampleParams& p);
+// one-shot event pair recorded around one kernel of the next negatives call
+void arm_profile(void* start_event, void* stop_event, int which);
 }  // namespace smore

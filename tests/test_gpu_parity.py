@@ -192,14 +192,15 @@ def test_accounting_variant_and_stage_split(qt):
     args = sm.make_args(300, 40, seed=4)
     out = sm.alloc_outputs(300, 40)
     sm.sample_positives(g, dag, args, out)
-    stats = torch.zeros((300, 2), dtype=torch.int64, device="cuda")
+    stats = torch.zeros((300, 4), dtype=torch.int64, device="cuda")
     sm.sample_negatives(g, dag, args, out, stats)
     got = to_numpy(out)
     for k in full:
         assert np.array_equal(full[k], got[k]), k
     st = stats.cpu().numpy()
     ok = got["n_valid"] >= 0
-    assert (st[ok] > 0).all() and (st[~ok] == 0).all() and (st[:, 1] * 64 >= st[:, 0] // 8).all()
+    assert (st[ok, 0] > 0).all() and (st[~ok] == 0).all() and (st >= 0).all()
+    assert (st[:, 1] * 64 >= st[:, 0] // 8).all() and (st[:, 3] * 64 >= st[:, 2] // 8).all()
 
 
 def test_negatives_on_caller_queries():

@@ -33,13 +33,21 @@ def test_freebase_sampled_rows_and_accounting():
         sm.sample_positives(g, dag, args, out)
         sm.sample_negatives(g, dag, args, out)
         got = to_numpy(out)
-        stats = torch.zeros((cfg.batch, 2), dtype=torch.int64, device="cuda")
+        stats = torch.zeros((cfg.batch, 4), dtype=torch.int64, device="cuda")
         sm.sample_negatives(g, dag, args, out, stats)
         counted = to_numpy(out)
         for k in FIELDS:
             assert np.array_equal(got[k], counted[k]), k
         st = stats.cpu().numpy()
         assert (st >= 0).all() and (st[got["n_valid"] >= 0, 0] > 0).all()
+        # the profiling hook records events around one kernel without changing rows
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        sm.profile_kernel(e0, e1, sm.KERNEL_CANDIDATES)
+        sm.sample_negatives(g, dag, args, out)
+        again = to_numpy(out)
+        for k in FIELDS:
+            assert np.array_equal(got[k], again[k]), k
+        assert e0.elapsed_time(e1) > 0
         rows = np.sort(rng.choice(cfg.batch, 24, replace=False))
         progress(f"{qt}: oracle on {len(rows)} sampled rows")
         ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
