@@ -40,20 +40,31 @@ def workload_name(cfg):
 
 
 def traffic_for(kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary (FETCH_SIZE scaled by the copy calibration, plus WRITE_SIZE),
-    or None when the summary was taken on other kernel sources."""
+    """HBM bytes per launch of `kernel` (e.g. "k_candidates<3p> r0") from the
+    committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE scaled by
+    a plain copy's readings), or None when there is none or it was taken on
+    other sources of the sampling kernels."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "counters_freebase.json")
+    path = os.path.join(ROOT, "profiles", "negatives_freebase_hbm_bytes.txt")
     if not os.path.exists(path):
         return None
+    fields, kernels = {}, {}
     with open(path) as f:
-        prof = json.load(f)
+        for line in f:
+            if line.startswith("#") or ":" not in line:
+                continue
+            key, val = line.split(":", 1)
+            if key == "kernel":
+                parts = [x.strip() for x in val.split("|")]
+                kernels[parts[0]] = int(parts[-1].split()[-1])
+            else:
+                fields[key.strip()] = val.strip()
     src = os.path.join(ROOT, "paper_2110_14890_amd", "csrc", "sample.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if prof.get("sample_hip_sha256_16") != sha or kernel not in prof.get("kernels", {}):
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    if fields.get("sample_hip_sha256_16") != sha:
         return None
-    return prof["kernels"][kernel]["hbm_bytes_per_launch"]
+    return kernels.get(kernel)
 
 
 def cpu_baseline(cfg, triples, types, seconds, threads):
@@ -225,7 +236,7 @@ def main():
     achieved = d["candidate_kernel_line_GBps"]
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 5),
-                "traffic": traffic_for(f"k_candidates<{dom}>"),
+                "traffic": traffic_for(f"k_candidates<{dom}> r0"),
                 "kernel": f"k_candidates<{dom}> (first round of smore_sample_negatives)",
                 "bytes_per_launch": acct[dom]["cand_lines"] * 64,
                 "useful_bytes_per_launch": acct[dom]["cand_bytes"],

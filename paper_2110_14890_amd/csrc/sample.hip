@@ -1,6 +1,6 @@
 // sample.hip -- query sampling with verified negatives on gfx950.
 //
-// Two kernels per call, on the caller's stream:
+// Positives (smore_sample_positives), one kernel:
 //
 //  k_positive: one thread per query.  Reverse directional sampling
 //    (Sec. 3.1; appendix on reverse directional sampling): attempt t grounds
@@ -10,17 +10,16 @@
 //    that reaches every anchor, keeps single-projection siblings apart and
 //    respects max_fanout wins.
 //
-//  k_verify<shape>: one workgroup per query.  Bidirectional rejection
-//    sampling (Sec. 3.2) at the node cut the planner picks for the shape:
-//    forward caching turns the anchors into their neighbour lists A_r(a)
-//    (sorted CSR groups, staged in LDS when small, used in place when not);
-//    candidates are drawn in rounds, one per lane, deduplicated against all
-//    earlier draws with an LDS hash table keyed by value holding the
-//    smallest draw index, and verified backward from the candidate.  A lane
-//    decides candidates whose backward lists are short; longer lists are
-//    queued and intersected by a whole wavefront (coalesced reads, ballot).
-//    Accepted candidates are compacted in draw order with wave ballots and
-//    per-row prefix sums, so the output does not depend on scheduling.
+// Negatives (smore_sample_negatives): bidirectional rejection sampling
+// (Sec. 3.2) at the node cut the planner picks for the shape, in rounds of
+// candidate draws; k_init and k_prepare once, then per round k_candidates,
+// k_heavy and k_compact, all on the caller's stream with no host
+// synchronisation in between (the kernels themselves are described where
+// they are defined).  Forward caching turns the anchors into their
+// neighbour lists A_r(a) (sorted CSR groups, staged in LDS when small, used
+// in place when not); each draw is verified backward from the candidate;
+// the first occurrences of the non-answers, in draw order, are the
+// negatives, so the output is a function of the draw indices alone.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -31,9 +30,6 @@
 namespace smore {
 namespace {
 
-constexpr int WG = 256;       // threads per verify workgroup
-constexpr int NW = WG / 64;   // wavefronts per workgroup
-constexpr int CHMAX = 512;    // candidates per round
 constexpr int STAGE = 1024;   // LDS entries per wavefront for staged forward lists
 constexpr int LANE_SEG = 8;   // backward lists up to this length stay on one lane
 
@@ -337,11 +333,12 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
 // --------------------------------------------------------------- negatives
 // Bidirectional rejection sampling of the negatives, in rounds of candidate
 // draws.  Per round:
-//   k_candidates  one lane per (query, draw): the draw, its cheap checks,
-//                 and either a decision or a push to the heavy queue;
+//   k_candidates  one wavefront per query: the round's draws, the in-edge
+//                 mask test, and for the survivors either a decision at lane
+//                 level or a push to the heavy queue;
 //   k_heavy       one wavefront per queued (query, draw): intersection of a
 //                 long backward list with the forward-cached list(s);
-//   k_compact     one workgroup per query: first-occurrence test of every
+//   k_compact     one wavefront per query: first-occurrence test of every
 //                 draw so far, ordered selection of the first n_neg kept.
 // Queries still short of n_neg after a round go to the next round through a
 // device-side list, so rounds need no host synchronisation.
