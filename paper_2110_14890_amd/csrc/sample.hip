@@ -898,6 +898,103 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out
     }
 }
 
+// The same selection for rounds of at most 64 * CK draws, with every load
+// in flight at once: each lane holds its CK draws (j = lane + 64 k) in
+// registers, one wavefront per query, four per workgroup, and only the
+// hash table lives in LDS.  Only non-answers enter the table: a value's
+// state is the same at each of its occurrences, so the first non-answer
+// occurrence of a value is its first occurrence.
+constexpr int CK = 16;
+constexpr int CWAVES = 4;
+
+template <int NK>
+__global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smore_sample_out out,
+                                                             Ws ws, int cur, int32_t j_end, int last,
+                                                             int32_t tcap, int tshift)
+{
+    extern __shared__ int32_t lds[];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t* tv = lds + (size_t)w * 2 * tcap;
+    int32_t* tj = tv + tcap;
+    const uint64_t below = lanes_below(lane);
+    const uint32_t tmask = (uint32_t)tcap - 1;
+    const int32_t nact = uni(ws.ctrl[2 + cur]);
+    if (blockIdx.x == 0 && threadIdx.x == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
+    const int32_t nk = uni((j_end + 63) >> 6);
+    for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
+        const int32_t b = uni(ws.act[cur][qi]);
+        const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
+        const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
+        int32_t* row = out.negatives + (int64_t)b * p.n_neg;
+        int32_t c[NK];
+        bool non[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            const int32_t j = 64 * k + lane;
+            c[k] = -1;
+            non[k] = false;
+            if (k < nk && j < j_end) {
+                c[k] = cv[j];
+                non[k] = sv[j] == ST_NON;
+            }
+        }
+        int4* t4 = (int4*)tv;
+        for (int32_t k = lane; k < tcap / 4; k += 64) {
+            t4[k] = make_int4(-1, -1, -1, -1);
+            ((int4*)tj)[k] = make_int4(INT_MAX, INT_MAX, INT_MAX, INT_MAX);
+        }
+        wave_sync();
+        // first probes of every draw in flight together; collisions probe on
+        uint32_t h[NK];
+        int32_t old[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            h[k] = ((uint32_t)c[k] * 0x9E3779B1u) >> tshift;
+            old[k] = non[k] ? atomicCAS(&tv[h[k]], -1, c[k]) : -1;
+        }
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            if (!non[k]) continue;
+            uint32_t at = h[k];
+            int32_t o = old[k];
+            while (o != -1 && o != c[k]) {
+                at = (at + 1) & tmask;
+                o = atomicCAS(&tv[at], -1, c[k]);
+            }
+            h[k] = at;
+            atomicMin(&tj[at], 64 * k + lane);
+        }
+        wave_sync();
+        int32_t first[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) first[k] = non[k] ? tj[h[k]] : -1;
+        int32_t acc = 0;
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            if (k >= nk || acc >= p.n_neg) break;
+            const int32_t j = 64 * k + lane;
+            const bool keep = non[k] && first[k] == j;
+            const uint64_t m = __ballot(keep);
+            const int32_t rank = acc + __popcll(m & below);
+            if (keep && rank < p.n_neg) {
+                row[rank] = c[k];
+                if (rank == p.n_neg - 1) out.neg_draws[b] = j + 1;
+            }
+            acc = uni(min(p.n_neg, acc + __popcll(m)));
+        }
+        if (acc == p.n_neg || last) {
+            for (int32_t k = acc + lane; k < p.n_neg; k += 64) row[k] = -1;
+            if (lane == 0) {
+                out.n_valid[b] = acc;
+                if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
+            }
+        } else if (lane == 0) {
+            ws.act[cur ^ 1][atomicAdd(&ws.ctrl[2 + (cur ^ 1)], 1)] = b;
+        }
+        wave_sync();   // the next query clears the table
+    }
+}
+
 __global__ void k_init(Ws ws)
 {
     for (int k = threadIdx.x; k < 64; k += blockDim.x) ws.ctrl[k] = 0;
@@ -962,6 +1059,20 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         const int32_t tcap = compact_tcap(j_end);
         int tshift = 32;
         for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
+        if (j_end <= 64 * CK) {
+            prof_mark(2, r, false, st);
+            const size_t tab = (size_t)CWAVES * 2 * tcap * sizeof(int32_t);
+            if (j_end <= 64 * 9)
+                k_compact_reg<9><<<PERSIST_BLOCKS, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                                                                          r == rounds - 1, tcap, tshift);
+            else
+                k_compact_reg<CK><<<PERSIST_BLOCKS, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                                                                           r == rounds - 1, tcap, tshift);
+            if ((rc = check_launch(err))) return rc;
+            prof_mark(2, r, true, st);
+            prev = j_end;
+            continue;
+        }
         const size_t lds = compact_lds(j_end);
         static bool attr = false;
         if (lds > 65536 && !attr) {
