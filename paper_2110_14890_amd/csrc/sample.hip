@@ -33,7 +33,10 @@ namespace {
 constexpr int STAGE = 1024;   // LDS entries per wavefront for staged forward lists
 constexpr int LANE_SEG = 8;   // backward lists up to this length stay on one lane
 
-enum : int32_t { ST_NON = 0, ST_ANS = 1, ST_DUP = 2, ST_PEND = 3 };
+// Draw states.  ST_DEEP exists only inside the candidate kernel: the
+// candidate's backward list is short and it is tested after the shallow
+// pass over all survivors of the window.
+enum : int32_t { ST_NON = 0, ST_ANS = 1, ST_DUP = 2, ST_PEND = 3, ST_DEEP = 4 };
 
 // Accounting of graph reads (bytes, and the 64-byte lines they span).  The
 // verification kernel is instantiated with Tally when the caller asks for
@@ -56,30 +59,83 @@ struct Tally {
     __device__ __forceinline__ void bytes_only(int64_t n) { b += (uint64_t)n; }
 };
 
-// Edges [x, y) of entity v under relation r in one direction ((0, 0) if
-// none).  Reads the node-pointer pair, the relations probed by the binary
-// search, and the group bounds.
+// Edges [x, y) of v under r when v's node-pointer pair (n0, n1) is known.
 template <class T>
-__device__ __forceinline__ int2 group_range(const DirView& d, int32_t v, int32_t r, T& tl)
+__device__ __forceinline__ int2 group_from(const DirView& d, int32_t n0, int32_t n1, int32_t r, T& tl)
 {
-    int32_t lo = d.node[v];
-    const int32_t end = d.node[v + 1];
-    tl.read(d.node + v, 8);
-    int32_t hi = end;
+    int32_t lo = n0, hi = n1;
     while (lo < hi) {
         const int32_t mid = (lo + hi) >> 1;
         tl.read(&d.grp[mid].x, 4);
         if (d.grp[mid].x < r) lo = mid + 1; else hi = mid;
     }
-    if (lo < end) {
-        const int2 gr = d.grp[lo];
-        if (gr.x == r) {
-            tl.read(&d.grp[lo].y, 4);
-            tl.read(&d.grp[lo + 1].y, 4);
-            return make_int2(gr.y, d.grp[lo + 1].y);
-        }
+    if (lo < n1 && d.grp[lo].x == r) {
+        tl.read(&d.grp[lo].y, 4);
+        tl.read(&d.grp[lo + 1].y, 4);
+        return make_int2(d.grp[lo].y, d.grp[lo + 1].y);
     }
     return make_int2(0, 0);
+}
+
+// group_from for an entity with at most SCAN groups: all of its group
+// entries (and the next one, for the end bound) are loaded at once, so the
+// lookup is one dependent step instead of a chain of binary-search probes.
+constexpr int SCAN = 8;
+
+template <class T>
+__device__ __forceinline__ int2 group_find(const DirView& d, int32_t n0, int32_t n1, int32_t r, T& tl)
+{
+    const int32_t n = n1 - n0;
+    if (n > SCAN) return group_from(d, n0, n1, r, tl);
+    if (n <= 0) return make_int2(0, 0);
+    int2 e[SCAN + 1];
+#pragma unroll
+    for (int k = 0; k <= SCAN; ++k) e[k] = k <= n ? d.grp[n0 + k] : make_int2(INT_MAX, 0);
+    tl.read(d.grp + n0, 8 * (n + 1));
+    int2 res = make_int2(0, 0);
+#pragma unroll
+    for (int k = 0; k < SCAN; ++k)
+        if (k < n && e[k].x == r) res = make_int2(e[k].y, e[k + 1].y);
+    return res;
+}
+
+// group_find of two entities at once (the loads of both scans in flight
+// together); inactive entries return (0, 0).
+template <class T>
+__device__ __forceinline__ void group_find2(const DirView& d, const int32_t* n0, const int32_t* n1,
+                                            const bool* act, int32_t r, int2* res, T& tl)
+{
+    int2 e[2][SCAN + 1];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int32_t n = act[u] ? n1[u] - n0[u] : 0;
+#pragma unroll
+        for (int k = 0; k <= SCAN; ++k)
+            e[u][k] = (n > 0 && n <= SCAN && k <= n) ? d.grp[n0[u] + k] : make_int2(INT_MAX, 0);
+        if (n > 0 && n <= SCAN) tl.read(d.grp + n0[u], 8 * (n + 1));
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int32_t n = act[u] ? n1[u] - n0[u] : 0;
+        res[u] = make_int2(0, 0);
+        if (n > SCAN) {
+            res[u] = group_from(d, n0[u], n1[u], r, tl);
+        } else {
+#pragma unroll
+            for (int k = 0; k < SCAN; ++k)
+                if (k < n && e[u][k].x == r) res[u] = make_int2(e[u][k].y, e[u][k + 1].y);
+        }
+    }
+}
+
+// Edges [x, y) of entity v under relation r in one direction ((0, 0) if
+// none): the node-pointer pair, then the group lookup.
+template <class T>
+__device__ __forceinline__ int2 group_range(const DirView& d, int32_t v, int32_t r, T& tl)
+{
+    const int32_t n0 = d.node[v], n1 = d.node[v + 1];
+    tl.read(d.node + v, 8);
+    return group_find(d, n0, n1, r, tl);
 }
 
 __device__ __forceinline__ int2 group_range(const DirView& d, int32_t v, int32_t r)
@@ -385,11 +441,11 @@ struct Ws {
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Round r covers draws [round_end(r-1), round_end(r)): first n_neg plus a
-// margin, then four times as many, up to neg_tries.
+// small margin (a query rarely rejects more than a few percent of its
+// draws), then four times as many, up to neg_tries.
 inline int32_t round_end(const SampleParams& p, int r)
 {
-    int64_t e = p.n_neg + p.n_neg / 16 + 32;
-    e = (e + 63) / 64 * 64;
+    int64_t e = p.n_neg + p.n_neg / 32 + 8;
     for (int k = 0; k < r; ++k) e *= 4;
     return (int32_t)(e < p.neg_tries ? e : p.neg_tries);
 }
@@ -453,24 +509,6 @@ __device__ __forceinline__ void flush_tally(T& tl, int64_t* stats, int32_t b, in
     }
 }
 
-// Edges [x, y) of v under r when v's node-pointer pair (n0, n1) is known.
-template <class T>
-__device__ __forceinline__ int2 group_from(const DirView& d, int32_t n0, int32_t n1, int32_t r, T& tl)
-{
-    int32_t lo = n0, hi = n1;
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        tl.read(&d.grp[mid].x, 4);
-        if (d.grp[mid].x < r) lo = mid + 1; else hi = mid;
-    }
-    if (lo < n1 && d.grp[lo].x == r) {
-        tl.read(&d.grp[lo].y, 4);
-        tl.read(&d.grp[lo + 1].y, 4);
-        return make_int2(d.grp[lo].y, d.grp[lo + 1].y);
-    }
-    return make_int2(0, 0);
-}
-
 // Is (a, r, c) an edge?  From the anchor's list when it is staged in LDS,
 // otherwise from c's reverse list under r (c's node pair already loaded).
 template <class T>
@@ -478,16 +516,18 @@ __device__ __forceinline__ bool edge_test(const GraphView& g, const FSet& Fa, in
                                           int32_t c, int32_t n0, int32_t n1, T& tl)
 {
     if (Fa.lds) return has(Fa, c, tl);
-    const int2 s = group_from(g.rev, n0, n1, r, tl);
+    const int2 s = group_find(g.rev, n0, n1, r, tl);
     return s.y > s.x && has(g.rev.nbr + s.x, s.y - s.x, a, true, tl);
 }
 
-// Decision for candidate c at lane level: ST_NON, ST_ANS, or ST_PEND when a
-// wavefront must intersect a long list.
+// First, shallow decision for candidate c at lane level: ST_NON or ST_ANS
+// when it is settled by the cached lists and c's own groups, ST_PEND when a
+// wavefront must intersect a long list, ST_DEEP with c's backward list
+// [lst.x, lst.y) when that list is short and is to be tested next.
 template <int QT, class T>
-__device__ __forceinline__ int32_t cand_test(const GraphView& g, const FSet* F, const int32_t* anc,
-                                             const int32_t* rel, int32_t c, int32_t n0, int32_t n1,
-                                             T& tl)
+__device__ __forceinline__ int32_t shallow_test(const GraphView& g, const FSet* F, const int32_t* anc,
+                                                const int32_t* rel, int32_t c, int32_t n0, int32_t n1,
+                                                int2& lst, T& tl)
 {
     if (QT == Q1P) return edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) ? ST_ANS : ST_NON;
     if (QT == Q2I)
@@ -503,23 +543,103 @@ __device__ __forceinline__ int32_t cand_test(const GraphView& g, const FSet* F, 
     if (QT == QPI && !edge_test(g, F[1], anc[1], rel[2], c, n0, n1, tl)) return ST_NON;
     // backward step from c under the relation entering the root
     const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
-    const int2 s = group_from(g.rev, n0, n1, rb, tl);
+    const int2 s = group_find(g.rev, n0, n1, rb, tl);
     if (s.y == s.x) return ST_NON;
-    const int32_t ns = s.y - s.x;
-    if (ns > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) return ST_PEND;
-    tl.read(g.rev.nbr + s.x, 4 * ns);
-    for (int32_t k = s.x; k < s.y; ++k) {
-        const int32_t y = g.rev.nbr[k];
-        if (QT == Q2P || QT == QPI) { if (has(F[0], y, tl)) return ST_ANS; }
-        else if (QT == QIP) { if (has(F[0], y, tl) && has(F[1], y, tl)) return ST_ANS; }
-        else if (QT == QUP) { if (has(F[0], y, tl) || has(F[1], y, tl)) return ST_ANS; }
-        else {  // 3p: second backward step from y under r1
-            const int2 s2 = group_range(g.rev, y, rel[1], tl);
-            if (s2.y - s2.x > LANE_SEG) return ST_PEND;
-            tl.read(g.rev.nbr + s2.x, 4 * (s2.y - s2.x));
-            for (int32_t m = s2.x; m < s2.y; ++m)
-                if (has(F[0], g.rev.nbr[m], tl)) return ST_ANS;
+    if (s.y - s.x > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) return ST_PEND;
+    lst = s;
+    return ST_DEEP;
+}
+
+// shallow_test of two candidates c[0], c[1] (act[u]: slot in use) with the
+// dependent steps of both interleaved.
+template <int QT, class T>
+__device__ __forceinline__ void shallow_test2(const GraphView& g, const FSet* F, const int32_t* anc,
+                                              const int32_t* rel, const int32_t* c, const bool* act,
+                                              int32_t* st, int2* lst, T& tl)
+{
+    int32_t n0[2], n1[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        n0[u] = n1[u] = 0;
+        if (act[u]) {
+            n0[u] = g.rev.node[c[u]];
+            n1[u] = g.rev.node[c[u] + 1];
+            tl.read(g.rev.node + c[u], 8);
         }
+    }
+    if (QT == Q1P || QT == Q2I || QT == Q3I || QT == Q2U) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            st[u] = act[u] ? shallow_test<QT>(g, F, anc, rel, c[u], n0[u], n1[u], lst[u], tl) : ST_NON;
+        return;
+    }
+    bool live[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        live[u] = act[u] && (QT != QPI || edge_test(g, F[1], anc[1], rel[2], c[u], n0[u], n1[u], tl));
+    const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
+    int2 sr[2];
+    group_find2(g.rev, n0, n1, live, rb, sr, tl);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        st[u] = ST_NON;
+        if (!live[u] || sr[u].y == sr[u].x) continue;
+        if (sr[u].y - sr[u].x > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) {
+            st[u] = ST_PEND;
+        } else {
+            lst[u] = sr[u];
+            st[u] = ST_DEEP;
+        }
+    }
+}
+
+// Then the deep decision: the backward list y[0..len) of c (len <= LANE_SEG)
+// against the staged forward list(s); for 3p one more backward step from
+// every y.
+template <int QT, class T>
+__device__ __forceinline__ int32_t deep_test(const GraphView& g, const FSet* F, const int32_t* rel,
+                                             int32_t start, int32_t len, T& tl)
+{
+    int32_t y[LANE_SEG];
+#pragma unroll
+    for (int k = 0; k < LANE_SEG; ++k) y[k] = k < len ? g.rev.nbr[start + k] : -1;
+    tl.read(g.rev.nbr + start, 4 * len);
+    if (QT != Q3P) {
+        bool hit = false;
+#pragma unroll
+        for (int k = 0; k < LANE_SEG; ++k) {
+            if (k >= len) break;
+            if (QT == Q2P || QT == QPI) hit = hit || has(F[0], y[k], tl);
+            else if (QT == QIP) hit = hit || (has(F[0], y[k], tl) && has(F[1], y[k], tl));
+            else hit = hit || has(F[0], y[k], tl) || has(F[1], y[k], tl);
+        }
+        return hit ? ST_ANS : ST_NON;
+    }
+    // 3p: node pairs of every y at once, then each y's group under r1
+    int32_t a0[LANE_SEG], a1[LANE_SEG];
+#pragma unroll
+    for (int k = 0; k < LANE_SEG; ++k) {
+        a0[k] = 0;
+        a1[k] = 0;
+        if (k < len) {
+            a0[k] = g.rev.node[y[k]];
+            a1[k] = g.rev.node[y[k] + 1];
+            tl.read(g.rev.node + y[k], 8);
+        }
+    }
+    for (int k = 0; k < len; ++k) {
+        const int2 s2 = group_find(g.rev, a0[k], a1[k], rel[1], tl);
+        const int32_t n2 = s2.y - s2.x;
+        if (n2 > LANE_SEG) return ST_PEND;
+        int32_t x[LANE_SEG];
+#pragma unroll
+        for (int m = 0; m < LANE_SEG; ++m) x[m] = m < n2 ? g.rev.nbr[s2.x + m] : -1;
+        tl.read(g.rev.nbr + s2.x, 4 * n2);
+        bool hit = false;
+#pragma unroll
+        for (int m = 0; m < LANE_SEG; ++m)
+            if (m < n2) hit = hit || has(F[0], x[m], tl);
+        if (hit) return ST_ANS;
     }
     return ST_NON;
 }
@@ -673,8 +793,9 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
 // loads in flight together); the draws with an in-edge are compacted into
 // the wave's survivor list and then verified one per lane, so a window
 // costs one dependent chain per 64 survivors instead of one per draw slot.
-constexpr int WIN = 512;
+constexpr int WIN = 576;
 constexpr int DPW = WIN / 64;
+static_assert(SMORE_MAX_NEG_TRIES <= 4096 && LANE_SEG <= 8, "deep items pack j and length in 15 bits");
 
 __device__ __forceinline__ void wave_sync()
 {
@@ -690,11 +811,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
 {
     __shared__ int32_t stage_all[CWG / 64][STAGE];
     __shared__ int32_t sc_all[CWG / 64][WIN];
-    __shared__ int32_t sj_all[CWG / 64][WIN];
+    __shared__ uint16_t sj_all[CWG / 64][WIN];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     int32_t* stage = stage_all[w];
     int32_t* sc = sc_all[w];
-    int32_t* sj = sj_all[w];
+    uint16_t* sj = sj_all[w];
     const uint64_t below = lanes_below(lane);
     const int32_t nact = uni(ws.ctrl[2 + cur]);
     const int32_t nwaves = gridDim.x * (CWG / 64);
@@ -756,20 +877,58 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 if (in) {
                     const int32_t at = nsurv + __popcll(m & below);
                     sc[at] = c[k];
-                    sj[at] = j;
+                    sj[at] = (uint16_t)j;
                 }
                 nsurv += __popcll(m);
             }
             wave_sync();
-            for (int32_t s0 = 0; s0 < nsurv; s0 += 64) {
-                if (s0 + lane < nsurv) {
-                    const int32_t cc = sc[s0 + lane], j = sj[s0 + lane];
-                    const int32_t n0 = g.rev.node[cc], n1 = g.rev.node[cc + 1];
-                    tl.read(g.rev.node + cc, 8);
-                    const int32_t st = cand_test<QT>(g, F, anc, rel, cc, n0, n1, tl);
+            // shallow pass over the survivors, 64 at a time; candidates with
+            // a short backward list are collected (in place, over entries
+            // already consumed) for one deep pass, so the dependent steps of
+            // the window's few deep candidates overlap
+            int32_t ndeep = 0;
+            for (int32_t s0 = 0; s0 < nsurv; s0 += 128) {
+                bool act[2];
+                int32_t cc[2], jj[2], st[2];
+                int2 lst[2] = {make_int2(0, 0), make_int2(0, 0)};
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int32_t at = s0 + 64 * u + lane;
+                    act[u] = at < nsurv;
+                    cc[u] = act[u] ? sc[at] : 0;
+                    jj[u] = act[u] ? sj[at] : 0;
+                }
+                wave_sync();
+                shallow_test2<QT>(g, F, anc, rel, cc, act, st, lst, tl);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    if (act[u] && st[u] != ST_DEEP) {
+                        sv[jj[u]] = (uint8_t)st[u];
+                        if (st[u] == ST_PEND) {
+                            const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers a round
+                            ws.queue[slot] = make_int2(b, jj[u]);
+                        }
+                    }
+                    const bool deep = act[u] && st[u] == ST_DEEP;
+                    const uint64_t m = __ballot(deep);
+                    if (deep) {
+                        // j < 4096 and 1 <= length <= 8 pack into 15 bits
+                        const int32_t at = ndeep + __popcll(m & below);
+                        sc[at] = lst[u].x;
+                        sj[at] = (uint16_t)((jj[u] << 3) | (lst[u].y - lst[u].x - 1));
+                    }
+                    ndeep += __popcll(m);
+                }
+            }
+            wave_sync();
+            for (int32_t d0 = 0; d0 < ndeep; d0 += 64) {
+                if (d0 + lane < ndeep) {
+                    const int32_t start = sc[d0 + lane], pk = sj[d0 + lane];
+                    const int32_t j = pk >> 3;
+                    const int32_t st = deep_test<QT>(g, F, rel, start, (pk & 7) + 1, tl);
                     sv[j] = (uint8_t)st;
                     if (st == ST_PEND) {
-                        const int32_t slot = atomicAdd(&ws.ctrl[0], 1);   // capacity covers a round
+                        const int32_t slot = atomicAdd(&ws.ctrl[0], 1);
                         ws.queue[slot] = make_int2(b, j);
                     }
                 }
