@@ -2,7 +2,8 @@
 //
 // Positives (smore_sample_positives), one kernel:
 //
-//  k_positive: one thread per query.  Reverse directional sampling
+//  k_positive: four lanes per query, each running every fourth attempt.
+//    Reverse directional sampling
 //    (Sec. 3.1; appendix on reverse directional sampling): attempt t grounds
 //    the root among entities with an in-edge, then runs the pre-order walk
 //    program compiled from the plan, each projection picking an in-relation
@@ -12,7 +13,7 @@
 //
 // Negatives (smore_sample_negatives): bidirectional rejection sampling
 // (Sec. 3.2) at the node cut the planner picks for the shape, in rounds of
-// candidate draws; k_init and k_prepare once, then per round k_candidates,
+// candidate draws; k_prepare once, then per round k_candidates,
 // k_heavy and k_compact, all on the caller's stream with no host
 // synchronisation in between (the kernels themselves are described where
 // they are defined).  Forward caching turns the anchors into their
@@ -315,74 +316,98 @@ __device__ __forceinline__ int32_t sel4(int i, int32_t a, int32_t b, int32_t c, 
     return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
 }
 
+// Attempts of one query run PA at a time, on PA neighbouring lanes (lane l
+// of the group takes attempts l, l + PA, ...): the lowest successful
+// attempt of a group step is the first successful attempt overall, so the
+// result is that of trying them one after the other.
+constexpr int PA = 4;
+
+// One attempt t of query q: true and the grounded registers when accepted.
+__device__ __forceinline__ bool pos_attempt(const GraphView& g, const WalkProgram& wp,
+                                            const SampleParams& p, uint32_t q, int t, int32_t* e,
+                                            int32_t* qr)
+{
+    e[0] = e[1] = e[2] = e[3] = -1;
+    qr[0] = qr[1] = qr[2] = -1;
+    if (g.n_active == 0) return false;
+    e[0] = g.active_in[reduce_range(draw64(p.seed, TAG_POS, q, t, 0), (uint32_t)g.n_active)];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k >= wp.n_steps) break;
+        const int32_t v = sel4(wp.src[k], e[0], e[1], e[2], e[3]);
+        const uint64_t u0 = draw64(p.seed, TAG_POS, q, t, 1 + 2 * k);
+        const uint64_t u1 = draw64(p.seed, TAG_POS, q, t, 2 + 2 * k);
+        const int32_t s0 = g.rev.node[v], s1 = g.rev.node[v + 1];
+        if (s0 == s1) return false;                       // no in-edge: dead end
+        const int32_t s = s0 + (int32_t)reduce_range(u0, (uint32_t)(s1 - s0));
+        const int2 gr = g.rev.grp[s];
+        const int32_t len = g.rev.grp[s + 1].y - gr.y;
+        const int32_t x = g.rev.nbr[gr.y + (int32_t)reduce_range(u1, (uint32_t)len)];
+        if (p.max_fanout > 0) {
+            const int2 fr = group_range(g.fwd, x, gr.x);
+            if (fr.y - fr.x > p.max_fanout) return false;
+        }
+        e[k + 1] = x;
+        qr[k] = gr.x;
+    }
+    for (int pr = 0; pr < wp.n_pairs; ++pr) {
+        const int32_t xa = sel4(wp.anchor_reg[wp.pair_anchor[pr][0]], e[0], e[1], e[2], e[3]);
+        const int32_t xb = sel4(wp.anchor_reg[wp.pair_anchor[pr][1]], e[0], e[1], e[2], e[3]);
+        int32_t ra = -1, rb = -1;
+        for (int k = 0; k < wp.n_steps; ++k) {
+            const int32_t rk = sel4(k, qr[0], qr[1], qr[2], -1);
+            if (wp.rel_slot[k] == wp.pair_rel[pr][0]) ra = rk;
+            if (wp.rel_slot[k] == wp.pair_rel[pr][1]) rb = rk;
+        }
+        if (xa == xb && ra == rb) return false;           // degenerate sibling branches
+    }
+    return true;
+}
+
 __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, SampleParams p,
                                                   smore_sample_out out)
 {
-    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= p.batch) return;
+    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t b = gid / PA;
+    const int l = gid % PA;
+    if (b >= p.batch) return;   // whole groups: PA divides the workgroup size
     const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
-    int32_t e0 = -1, e1 = -1, e2 = -1, e3 = -1;   // registers: root, then one per step
-    int32_t q0 = -1, q1 = -1, q2 = -1;            // relation grounded by step k
-    int t = 0;
-    bool found = false;
-    for (; t < p.pos_tries && !found; ++t) {
-        if (g.n_active == 0) continue;
-        e0 = g.active_in[reduce_range(draw64(p.seed, TAG_POS, q, t, 0), (uint32_t)g.n_active)];
-        bool ok = true;
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-            if (!ok || k >= wp.n_steps) break;
-            const int32_t e = sel4(wp.src[k], e0, e1, e2, e3);
-            const uint64_t u0 = draw64(p.seed, TAG_POS, q, t, 1 + 2 * k);
-            const uint64_t u1 = draw64(p.seed, TAG_POS, q, t, 2 + 2 * k);
-            const int32_t s0 = g.rev.node[e], s1 = g.rev.node[e + 1];
-            if (s0 == s1) { ok = false; break; }          // no in-edge: dead end
-            const int32_t s = s0 + (int32_t)reduce_range(u0, (uint32_t)(s1 - s0));
-            const int2 gr = g.rev.grp[s];
-            const int32_t len = g.rev.grp[s + 1].y - gr.y;
-            const int32_t x = g.rev.nbr[gr.y + (int32_t)reduce_range(u1, (uint32_t)len)];
-            if (p.max_fanout > 0) {
-                const int2 fr = group_range(g.fwd, x, gr.x);
-                if (fr.y - fr.x > p.max_fanout) { ok = false; break; }
-            }
-            if (k == 0) { e1 = x; q0 = gr.x; }
-            if (k == 1) { e2 = x; q1 = gr.x; }
-            if (k == 2) { e3 = x; q2 = gr.x; }
+    const int gbase = (threadIdx.x & 63) & ~(PA - 1);
+    int32_t e[4], qr[3];
+    int win = -1;
+    for (int t0 = 0; t0 < p.pos_tries; t0 += PA) {
+        const int t = t0 + l;
+        const bool ok = t < p.pos_tries && pos_attempt(g, wp, p, q, t, e, qr);
+        const uint32_t m = (uint32_t)(__ballot(ok) >> gbase) & ((1u << PA) - 1);
+        if (m) {
+            win = t0 + __ffs(m) - 1;
+            break;
         }
-        if (ok) {
-            for (int pr = 0; pr < wp.n_pairs; ++pr) {
-                const int32_t xa = sel4(wp.anchor_reg[wp.pair_anchor[pr][0]], e0, e1, e2, e3);
-                const int32_t xb = sel4(wp.anchor_reg[wp.pair_anchor[pr][1]], e0, e1, e2, e3);
-                int32_t ra = -1, rb = -1;
-                for (int k = 0; k < wp.n_steps; ++k) {
-                    const int32_t rk = sel4(k, q0, q1, q2, -1);
-                    if (wp.rel_slot[k] == wp.pair_rel[pr][0]) ra = rk;
-                    if (wp.rel_slot[k] == wp.pair_rel[pr][1]) rb = rk;
-                }
-                if (xa == xb && ra == rb) ok = false;      // degenerate sibling branches
-            }
-        }
-        found = ok;
     }
-    int32_t* A = out.anchors + 3 * (int64_t)b;
-    int32_t* R = out.relations + 3 * (int64_t)b;
-    if (!found) {
-        for (int k = 0; k < 3; ++k) { A[k] = -1; R[k] = -1; }
-        out.positive[b] = -1;
-        out.n_valid[b] = -1;
-        out.pos_attempts[b] = p.pos_tries;
+    if (win < 0) {
+        if (l == 0) {
+            int32_t* A = out.anchors + 3 * (int64_t)b;
+            int32_t* R = out.relations + 3 * (int64_t)b;
+            for (int k = 0; k < 3; ++k) { A[k] = -1; R[k] = -1; }
+            out.positive[b] = -1;
+            out.n_valid[b] = -1;
+            out.pos_attempts[b] = p.pos_tries;
+        }
         return;
     }
-    for (int a = 0; a < 3; ++a) A[a] = a < wp.n_anchor ? sel4(wp.anchor_reg[a], e0, e1, e2, e3) : -1;
-    for (int s = 0; s < 3; ++s) {
+    if (l != win % PA) return;  // the lane that ran the winning attempt writes the row
+    int32_t* A = out.anchors + 3 * (int64_t)b;
+    int32_t* R = out.relations + 3 * (int64_t)b;
+    for (int a = 0; a < 3; ++a) A[a] = a < wp.n_anchor ? sel4(wp.anchor_reg[a], e[0], e[1], e[2], e[3]) : -1;
+    for (int sl = 0; sl < 3; ++sl) {
         int32_t v = -1;
         for (int k = 0; k < wp.n_steps; ++k)
-            if (wp.rel_slot[k] == s) v = sel4(k, q0, q1, q2, -1);
-        R[s] = v;
+            if (wp.rel_slot[k] == sl) v = sel4(k, qr[0], qr[1], qr[2], -1);
+        R[sl] = v;
     }
-    out.positive[b] = e0;
+    out.positive[b] = e[0];
     out.n_valid[b] = 0;
-    out.pos_attempts[b] = t;      // t was advanced past the accepted attempt
+    out.pos_attempts[b] = win + 1;
 }
 
 
@@ -748,14 +773,23 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
 {
     const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= p.batch) return;
+    if (b == 0) {   // queue and list counters of the first round: every query is listed
+        ws.ctrl[0] = 0;
+        ws.ctrl[1] = 0;
+        ws.ctrl[2] = p.batch;
+        ws.ctrl[3] = 0;
+    }
+    ws.act[0][b] = b;
     int32_t anc[3], rel[3];
     int32_t* row = out.negatives + (int64_t)b * p.n_neg;
+    int32_t* q = ws.qf + (int64_t)b * QF;
     if (stats)
         for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
     if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
         for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
         out.n_valid[b] = -1;
         out.neg_draws[b] = -1;
+        q[6] = -1;   // skipped by the rounds
         return;
     }
     if (p.n_neg == 0) {
@@ -764,7 +798,6 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
         return;
     }
     T tl;
-    int32_t* q = ws.qf + (int64_t)b * QF;
     int32_t used = 0, staged = 0;
     for (int f = 0; f < Shape<QT>::nf; ++f) {
         const int2 r = group_range(g.fwd, anc[Shape<QT>::fa[f]], rel[Shape<QT>::fr[f]], tl);
@@ -779,7 +812,6 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
         if (Shape<QT>::cached[f] || (staged >> f & 1)) tl.read(g.fwd.nbr + r.x, 4 * n);
     }
     q[6] = staged;
-    ws.act[0][atomicAdd(&ws.ctrl[2], 1)] = b;
     if constexpr (T::on) {
         stats[4 * (int64_t)b] = (int64_t)tl.b;
         stats[4 * (int64_t)b + 1] = (int64_t)tl.l;
@@ -830,6 +862,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
         }
         const int32_t* qb = ws.qf + (int64_t)b * QF;
         const int32_t staged = uni(qb[6]);
+        if (staged < 0) continue;   // query without a valid positive
         FSet F[3];
         int32_t used = 0;
 #pragma unroll
@@ -1016,6 +1049,7 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out
     if (blockIdx.x == 0 && lane == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
     for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
         const int32_t b = uni(ws.act[cur][qi]);
+        if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
         const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
@@ -1082,6 +1116,7 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
     const int32_t nk = uni((j_end + 63) >> 6);
     for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
         const int32_t b = uni(ws.act[cur][qi]);
+        if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
         const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
@@ -1154,11 +1189,6 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
     }
 }
 
-__global__ void k_init(Ws ws)
-{
-    for (int k = threadIdx.x; k < 64; k += blockDim.x) ws.ctrl[k] = 0;
-}
-
 // first-occurrence table of the compaction: load factor at most 0.6
 inline int32_t compact_tcap(int32_t j_end)
 {
@@ -1198,7 +1228,6 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                   int64_t* stats, int32_t R, hipStream_t st, const char** err)
 {
     int rc;
-    k_init<<<1, 64, 0, st>>>(ws);
     k_prepare<QT, T><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, out, ws, stats, R);
     if ((rc = check_launch(err))) return rc;
     if (p.n_neg == 0) return SMORE_OK;
@@ -1207,12 +1236,15 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
         const int32_t j_end = round_end(p, r);
+        // later rounds carry the few queries short of n_neg: a smaller grid
+        // keeps their (often empty) launches cheap
+        const int grid = r == 0 ? PERSIST_BLOCKS : PERSIST_BLOCKS / 4;
         prof_mark(0, r, false, st);
-        k_candidates<QT, T><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
+        k_candidates<QT, T><<<grid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
         if ((rc = check_launch(err))) return rc;
         prof_mark(0, r, true, st);
         prof_mark(1, r, false, st);
-        k_heavy<QT, T><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
+        k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
         prof_mark(1, r, true, st);
         const int32_t tcap = compact_tcap(j_end);
@@ -1222,10 +1254,10 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             prof_mark(2, r, false, st);
             const size_t tab = (size_t)CWAVES * 2 * tcap * sizeof(int32_t);
             if (j_end <= 64 * 9)
-                k_compact_reg<9><<<PERSIST_BLOCKS, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                k_compact_reg<9><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
                                                                           r == rounds - 1, tcap, tshift);
             else
-                k_compact_reg<CK><<<PERSIST_BLOCKS, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                k_compact_reg<CK><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
                                                                            r == rounds - 1, tcap, tshift);
             if ((rc = check_launch(err))) return rc;
             prof_mark(2, r, true, st);
@@ -1242,7 +1274,7 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             attr = true;
         }
         prof_mark(2, r, false, st);
-        k_compact<<<PERSIST_BLOCKS * 4, 64, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
+        k_compact<<<grid * 4, 64, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
                                                        tshift);
         if ((rc = check_launch(err))) return rc;
         prof_mark(2, r, true, st);
@@ -1298,7 +1330,9 @@ size_t negatives_workspace_bytes(const SampleParams& p)
 int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
                     const smore_sample_out& out, hipStream_t st, const char** err)
 {
-    k_positive<<<(p.batch + 255) / 256, 256, 0, st>>>(view_of(g), wp, p, out);
+    static_assert(256 % PA == 0 && (PA & (PA - 1)) == 0, "attempt groups tile the workgroup");
+    const int64_t threads = (int64_t)p.batch * PA;
+    k_positive<<<(unsigned)((threads + 255) / 256), 256, 0, st>>>(view_of(g), wp, p, out);
     return check_launch(err);
 }
 
