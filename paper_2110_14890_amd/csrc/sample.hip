@@ -447,6 +447,17 @@ SHAPE(Q2U, 2, 2, 2, 0, 1, 0, 0, 1, 0, 0, 0, 0)
 SHAPE(QUP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
 #undef SHAPE
 
+// Lists that test a candidate by one edge into the root: c is an answer
+// only if c is in list f for every f of `mask` (any f when `any`).  When
+// these lists are staged in LDS they decide the draws without a single
+// graph read; otherwise the in-edge mask does.
+template <int QT> struct RootLists { static constexpr int mask = 0, any = 0; };
+template <> struct RootLists<Q1P> { static constexpr int mask = 1, any = 0; };
+template <> struct RootLists<Q2I> { static constexpr int mask = 3, any = 0; };
+template <> struct RootLists<Q3I> { static constexpr int mask = 7, any = 0; };
+template <> struct RootLists<QPI> { static constexpr int mask = 2, any = 0; };
+template <> struct RootLists<Q2U> { static constexpr int mask = 3, any = 1; };
+
 constexpr int CWG = 256;         // threads of the candidate and compaction workgroups
 constexpr int HEAVY_WG = 256;    // threads of the heavy-queue workgroups
 constexpr int QF = 8;            // int32 per query in the per-query block
@@ -879,6 +890,10 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
         }
         int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
+        // first test of every draw: the staged root-edge lists when the
+        // shape has them (LDS only), else the in-edge mask
+        constexpr int RM = RootLists<QT>::mask;
+        const bool use_lists = RM != 0 && (RootLists<QT>::any ? (staged & RM) == RM : (staged & RM) != 0);
         for (int32_t base = j0; base < j1; base += WIN) {
             // Every answer of every shape is reached by a projection, so a
             // draw without an in-edge is a non-answer: the in-edge mask (V
@@ -892,7 +907,20 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 word[k] = 0;
                 if (j < j1) {
                     c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
-                    word[k] = g.has_in[c[k] >> 5];
+                    if (!use_lists) word[k] = g.has_in[c[k] >> 5];
+                }
+            }
+            if (use_lists) {
+#pragma unroll
+                for (int k = 0; k < DPW; ++k) {
+                    bool hit = !RootLists<QT>::any;
+#pragma unroll
+                    for (int f = 0; f < 3; ++f) {
+                        if (!(RM >> f & 1) || !(staged >> f & 1)) continue;
+                        const bool h = has(F[f], c[k], tl);
+                        hit = RootLists<QT>::any ? (hit || h) : (hit && h);
+                    }
+                    word[k] = hit ? ~0u : 0u;
                 }
             }
             int32_t nsurv = 0;
@@ -902,7 +930,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 const bool live = j < j1;
                 const bool in = live && ((word[k] >> (c[k] & 31)) & 1u);
                 if (live) {
-                    tl.read(g.has_in + (c[k] >> 5), 4);
+                    if (!use_lists) tl.read(g.has_in + (c[k] >> 5), 4);
                     cv[j] = c[k];
                     if (!in) sv[j] = ST_NON;
                 }
