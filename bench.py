@@ -67,6 +67,36 @@ def traffic_for(kernel):
     return kernels.get(kernel)
 
 
+def gather_ceiling(stream):
+    """Random-read ceiling of this GPU at several table footprints: the
+    library's probe kernel (smore_gather_probe) makes 2^26 random 4-byte
+    reads, eight in flight per lane.  Every read that misses L2 moves a
+    128-byte line, so reads/s x 128 B is the memory traffic; the sampler's
+    gathers are reads of the same kind."""
+    import torch
+
+    import paper_2110_14890_amd as sm
+
+    res = []
+    n = 1 << 26
+    for mib in (16, 1024, 4096):
+        x = torch.ones(mib * (1 << 20) // 4, dtype=torch.int32, device="cuda")
+        sm.gather_probe(x, n, stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(5):
+            sm.gather_probe(x, n, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 5 / 1e3
+        res.append({"footprint_MiB": mib, "G_reads_per_s": round(n / t / 1e9, 2),
+                    "line_GBps_128B": round(n * 128 / t / 1e9, 1)})
+        del x
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(cfg, triples, types, seconds, threads):
     """The CPU oracle, timed on the host on the first queries of each shape
     (a bounded sample of the same workload)."""
@@ -108,6 +138,7 @@ def main():
     ap.add_argument("--types", default=None, help="comma list; default: the workload's shapes")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gather-ceiling", action="store_true")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -246,6 +277,10 @@ def main():
                               "probes, group bounds, short backward lists, forward lists staged "
                               "once per query), times 64, summed over the launch"}
 
+    ceiling = None if args.no_gather_ceiling else gather_ceiling(stream)
+    if ceiling:
+        log(f"random-read ceiling: {ceiling}")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, triples, types, args.cpu_seconds, threads)
@@ -260,6 +295,7 @@ def main():
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "gather_ceiling": ceiling,
         "per_type": {qt: {k: (round(v, 4) if isinstance(v, float) else v)
                           for k, v in per_type[qt].items()} for qt in types},
         "graph_build_s": round(build_s, 3),

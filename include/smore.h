@@ -198,6 +198,18 @@ int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
    caller.  Returns SMORE_E_INVALID_ARG for another `which`. */
 int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
 
+/* Instrumentation: n_reads random 4-byte reads from the device table of
+   table_bytes (the first word of pseudo-randomly chosen 64-byte lines among
+   the largest power-of-two number of lines that fits), eight independent
+   reads in flight per lane, folded into sink (device uint32, at least
+   (n_reads + 63) / 64 words, overwritten).  The rate of this kernel is the
+   device's random-read ceiling that the sampler's gathers are compared
+   with; it is not part of sampling.  Asynchronous on hip_stream.  Errors:
+   SMORE_E_INVALID_ARG for null pointers, a table under 64 bytes, n_reads
+   outside [1, 2^40] or a short sink. */
+int smore_gather_probe(const void *table, int64_t table_bytes, int64_t n_reads, uint32_t *sink,
+                       int64_t sink_words, void *hip_stream);
+
 /* Release a graph (NULL is a no-op). */
 void smore_free_graph(smore_graph *g);
 

@@ -84,6 +84,7 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp, c_vp, ctypes.c_size_t, c_vp]
         L.smore_profile_kernel.argtypes = [c_vp, c_vp, c_i32]
+        L.smore_gather_probe.argtypes = [c_vp, c_i64, c_i64, c_vp, c_i64, c_vp]
         L.smore_free_graph.argtypes = [c_vp]
         L.smore_free_graph.restype = None
         _lib = L
@@ -271,3 +272,17 @@ def sample(graph: Graph, qtype: "str | QueryDag", batch: int, n_neg: int, seed: 
     args = make_args(batch, n_neg, seed, query_offset, pos_tries, neg_tries, max_fanout)
     out = alloc_outputs(batch, n_neg)
     return sample_into(graph, dag, args, out, stream)
+
+
+def gather_probe(table, n_reads: int, stream=None):
+    """Random-read ceiling probe (smore_gather_probe): n_reads random 4-byte
+    reads from the device tensor `table`.  Returns the sink tensor; time it
+    with events on `stream`."""
+    import torch
+
+    threads = (n_reads + 63) // 64
+    sink = torch.empty(threads, dtype=torch.int32, device=table.device)
+    st = stream if stream is not None else torch.cuda.current_stream(table.device)
+    _check(lib().smore_gather_probe(c_vp(table.data_ptr()), table.numel() * table.element_size(),
+                                    n_reads, c_vp(sink.data_ptr()), threads, c_vp(st.cuda_stream)))
+    return sink

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsmore.so")
-SOURCES = ["capi.cpp", "graph_build.hip", "sample.hip"]
+SOURCES = ["capi.cpp", "graph_build.hip", "sample.hip", "probe.hip"]
 ARCH = os.environ.get("SMORE_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [

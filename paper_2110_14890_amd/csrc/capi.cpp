@@ -337,6 +337,20 @@ int smore_profile_kernel(void* start_event, void* stop_event, int32_t which)
     return ok();
 }
 
+int smore_gather_probe(const void* table, int64_t table_bytes, int64_t n_reads, uint32_t* sink,
+                       int64_t sink_words, void* hip_stream)
+{
+    if (!table || !sink) return fail(SMORE_E_INVALID_ARG, "table and sink are required");
+    if (table_bytes < 64) return fail(SMORE_E_INVALID_ARG, "table_bytes must be at least 64");
+    if (n_reads < 1 || n_reads > ((int64_t)1 << 40)) return fail(SMORE_E_INVALID_ARG, "n_reads out of range");
+    if (sink_words < smore::gather_probe_threads(n_reads))
+        return fail(SMORE_E_INVALID_ARG, "sink needs %lld words", (long long)smore::gather_probe_threads(n_reads));
+    const char* err = nullptr;
+    const int rc = smore::launch_gather_probe(table, table_bytes, n_reads, sink, (hipStream_t)hip_stream, &err);
+    if (rc) return fail(rc, "%s", err ? err : "launch failed");
+    return ok();
+}
+
 void smore_free_graph(smore_graph* g)
 {
     if (!g) return;

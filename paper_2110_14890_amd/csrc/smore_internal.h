@@ -77,4 +77,7 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
 size_t negatives_workspace_bytes(const SampleParams& p);
 // one-shot event pair recorded around one kernel of the next negatives call
 void arm_profile(void* start_event, void* stop_event, int which);
+int64_t gather_probe_threads(int64_t n_reads);
+int launch_gather_probe(const void* table, int64_t table_bytes, int64_t n_reads, uint32_t* sink,
+                        hipStream_t st, const char** err);
 }  // namespace smore

@@ -224,3 +224,13 @@ def test_workspace_bytes(L):
     bad.neg_tries = 1
     n = ctypes.c_size_t()
     _expect(L.smore_sample_workspace_bytes(None, ctypes.byref(dag), ctypes.byref(bad), ctypes.byref(n)), -1)
+
+
+def test_gather_probe_validation_on_host(L):
+    vp = ctypes.c_void_p
+    fake = vp(0x1000)
+    assert L.smore_gather_probe(None, 1 << 20, 64, fake, 1, None) == -1
+    assert L.smore_gather_probe(fake, 32, 64, fake, 1, None) == -1           # table under one line
+    assert L.smore_gather_probe(fake, 1 << 20, 0, fake, 1, None) == -1       # no reads
+    assert L.smore_gather_probe(fake, 1 << 20, 6400, fake, 99, None) == -1   # sink needs 100 words
+    assert b"sink" in L.smore_last_error()

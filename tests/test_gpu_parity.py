@@ -222,3 +222,17 @@ def test_negatives_on_caller_queries():
     for k in ("negatives", "n_valid", "neg_draws"):
         assert np.array_equal(got[k][keep], ref[k][keep]), k
     assert (got["n_valid"][[5, 6]] == -1).all() and (got["negatives"][[5, 6]] == -1).all()
+
+
+def test_gather_probe_reads_the_table():
+    import torch
+    # every word of a table of ones: 64 reads per lane fold to zero; of
+    # twos-and-ones the fold is not constant, which shows the reads happen
+    t = torch.ones(1 << 20, dtype=torch.int32, device="cuda")
+    s = sm.gather_probe(t, 1 << 16)
+    torch.cuda.synchronize()
+    assert s.numel() == 1024 and (s == 0).all()
+    t[::3] = 2
+    s = sm.gather_probe(t, 1 << 16)
+    torch.cuda.synchronize()
+    assert (s != 0).any()
