@@ -97,6 +97,66 @@ def gather_ceiling(stream):
     return res
 
 
+def c_sweep(cfg, triples, g, threads, stream, seconds):
+    """Time to sample one minibatch of 1,024 queries as a function of the
+    maximum expansion C per relation (Sec. 5.2, sampler speed; the paper's
+    plots vary C on Freebase for 2p and ip): the GPU bidirectional sampler
+    against the exhaustive CPU oracle on the same minibatches.  C bounds the
+    width of every grounded step of the positive (max_fanout, rejection).
+    The oracle runs until `seconds` per point, then its rate is
+    extrapolated to the minibatch; the rows it produced are compared with
+    the GPU's.  One JSON line per (shape, C)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2110_14890_amd as sm
+
+    t0 = time.time()
+    og = oracle.Graph(triples, cfg.n_entities, cfg.n_relations, cfg.add_inverse, threads=threads)
+    log(f"oracle graph built in {time.time() - t0:.1f} s")
+    mb, reps = 1024, 10
+    for qt in ("2p", "ip"):
+        dag = sm.query_preset(qt)
+        for C in (10, 30, 100, 300, 1000, 3000, 0):
+            args = [sm.make_args(mb, cfg.n_neg, seed=cfg.seed, query_offset=k * mb, max_fanout=C)
+                    for k in range(reps + 2)]
+            outs = [sm.alloc_outputs(mb, cfg.n_neg) for _ in range(reps + 2)]
+            for k in range(2):
+                sm.sample_into(g, dag, args[k], outs[k], stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for k in range(2, reps + 2):
+                sm.sample_into(g, dag, args[k], outs[k], stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gpu_ms = e0.elapsed_time(e1) / reps
+            # the oracle on the first timed minibatch, in chunks, within the budget
+            got = {k: v.cpu().numpy() for k, v in outs[2].items()}
+            done, spent, chunk, same = 0, 0.0, threads, True
+            while done < mb and spent < seconds:
+                c = min(chunk, mb - done)
+                t = time.time()
+                ref = og.sample(qt, c, cfg.n_neg, seed=cfg.seed, query_offset=2 * mb + done,
+                                max_fanout=C, threads=threads)
+                spent += time.time() - t
+                for k in sm.OUT_FIELDS:
+                    same = same and np.array_equal(got[k][done:done + c], ref[k])
+                done += c
+                chunk = min(chunk * 2, 8 * threads)
+            cpu_ms = spent / done * mb * 1e3
+            line = {"sweep": "max_expansion_C", "shape": qt, "C": C if C else None,
+                    "minibatch": mb, "n_neg": cfg.n_neg, "gpu_ms_per_minibatch": round(gpu_ms, 4),
+                    "oracle_ms_per_minibatch": round(cpu_ms, 1),
+                    "oracle_queries_run": done, "oracle_extrapolated": done < mb,
+                    "oracle_threads": threads, "speedup": round(cpu_ms / gpu_ms, 1),
+                    "rows_identical": bool(same),
+                    "valid_queries": int((got["n_valid"] >= 0).sum())}
+            print(json.dumps(line), flush=True)
+    del og
+
+
 def cpu_baseline(cfg, triples, types, seconds, threads):
     """The CPU oracle, timed on the host on the first queries of each shape
     (a bounded sample of the same workload)."""
@@ -139,6 +199,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-ceiling", action="store_true")
+    ap.add_argument("--c-sweep", action="store_true",
+                    help="instead of the benchmark: minibatch time vs max expansion C, "
+                         "GPU vs the exhaustive CPU oracle (2p, ip)")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -185,6 +248,9 @@ def main():
         f"S_rev={g.S_rev:,} {g.device_bytes / 1e9:.2f} GB")
 
     stream = torch.cuda.current_stream()
+    if args.c_sweep:
+        c_sweep(cfg, triples, g, threads, stream, args.cpu_seconds)
+        return
     neg_tries = 4 * cfg.n_neg
     dags = {qt: sm.query_preset(qt) for qt in types}
     argv = {qt: sm.make_args(cfg.batch, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries) for qt in types}

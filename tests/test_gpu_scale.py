@@ -3,7 +3,8 @@ triples), in the launch configuration bench.py times: the whole batch of
 16,384 queries x 512 negatives runs on the GPU; the oracle recomputes a
 random sample of rows one query at a time (its exhaustive answer sets make
 every query cost up to seconds here).  Also checks that the read-accounting
-variant of the verification kernel returns the same rows."""
+variant of the verification kernel returns the same rows, and minibatches
+of 1,024 queries with a maximum expansion per relation."""
 import numpy as np
 import pytest
 
@@ -13,18 +14,25 @@ from gpu_common import (FIELDS, assert_same, config_graph, graph_pair, oracle_ro
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.timeout(900)
-def test_freebase_sampled_rows_and_accounting():
+@pytest.fixture(scope="module")
+def freebase():
     require_gpu()
-    import torch
-
-    import paper_2110_14890_amd as sm
-
     progress("generating the Freebase-shaped graph")
     cfg, tr = config_graph("freebase")
     progress(f"{len(tr):,} triples; building device and oracle graphs")
     g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
     del tr
+    yield cfg, g, og
+    g.close()
+
+
+@pytest.mark.timeout(900)
+def test_freebase_sampled_rows_and_accounting(freebase):
+    import torch
+
+    import paper_2110_14890_amd as sm
+
+    cfg, g, og = freebase
     rng = np.random.default_rng(1)
     for qt in cfg.query_types:
         dag = sm.query_preset(qt)
@@ -53,3 +61,23 @@ def test_freebase_sampled_rows_and_accounting():
         ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
         assert_same(got, ref, rows=rows, what=f"freebase/{qt}")
         progress(f"{qt}: ok, {int((got['n_valid'] == cfg.n_neg).sum())} complete queries")
+        del stats
+
+
+@pytest.mark.timeout(900)
+def test_freebase_max_expansion_minibatches(freebase):
+    """Minibatches of 1,024 queries with a maximum expansion C per relation
+    (max_fanout; the sampler-speed experiment of Sec. 5.2 varies C on
+    Freebase for 2p and ip): sampled rows against the oracle."""
+    import paper_2110_14890_amd as sm
+
+    cfg, g, og = freebase
+    rng = np.random.default_rng(2)
+    for qt in ("2p", "ip"):
+        for C in (10, 300):
+            got = to_numpy(sm.sample(g, qt, 1024, cfg.n_neg, seed=cfg.seed, query_offset=4096,
+                                     max_fanout=C))
+            rows = np.sort(rng.choice(1024, 24, replace=False))
+            ref = oracle_rows(og, qt, rows + 4096, cfg.n_neg, cfg.seed, 4 * cfg.n_neg, max_fanout=C)
+            assert_same(got, ref, rows=rows, what=f"freebase/{qt}/C={C}")
+            progress(f"{qt} C={C}: ok, {int((got['n_valid'] >= 0).sum())} queries with a positive")
