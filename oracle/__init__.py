@@ -71,6 +71,8 @@ def lib():
         L.oracle_graph_active_in.argtypes = [P, P]
         L.oracle_sample.argtypes = [P, ctypes.c_int, ctypes.POINTER(_Args), P, P, P, P, P, P, P,
                                     ctypes.c_int]
+        L.oracle_sample_shared.argtypes = [P, ctypes.c_int, ctypes.POINTER(_Args), P, P, P, P, P, P,
+                                           P, P, ctypes.c_int]
         L.oracle_answer_set.restype = ctypes.c_int64
         L.oracle_answer_set.argtypes = [P, ctypes.c_int, P, P, P, ctypes.c_int64]
         L.oracle_bidir_check.argtypes = [P, ctypes.c_int, P, P, ctypes.c_uint32, ctypes.c_int32, P]
@@ -193,4 +195,30 @@ class Graph:
                                  out["neg_draws"].ctypes.data, threads)
         if rc != 0:
             raise ValueError("oracle_sample rejected its arguments")
+        return out
+
+    def sample_shared(self, qtype: str, batch: int, n_shared: int, seed: int = 0,
+                      query_offset: int = 0, pos_tries: int = 64, neg_tries: int | None = None,
+                      max_fanout: int = 0, threads: int = 0):
+        """Minibatch with one shared candidate set (oracle_sample_shared)."""
+        if neg_tries is None:
+            neg_tries = 4 * n_shared
+        a = _Args(batch, n_shared, pos_tries, neg_tries, max_fanout, seed, query_offset)
+        words = (n_shared + 31) // 32
+        out = {
+            "anchors": np.zeros((batch, 3), np.int32),
+            "relations": np.zeros((batch, 3), np.int32),
+            "positive": np.zeros(batch, np.int32),
+            "pos_attempts": np.zeros(batch, np.int32),
+            "shared": np.zeros(n_shared, np.int32),
+            "n_shared": np.zeros(1, np.int32),
+            "mask": np.zeros((batch, words), np.uint32),
+            "n_valid": np.zeros(batch, np.int32),
+        }
+        rc = lib().oracle_sample_shared(self._h, TYPES.index(qtype), ctypes.byref(a),
+                                        *[out[k].ctypes.data for k in
+                                          ("anchors", "relations", "positive", "pos_attempts",
+                                           "shared", "n_shared", "mask", "n_valid")], threads)
+        if rc != 0:
+            raise ValueError("oracle_sample_shared rejected its arguments")
         return out

@@ -60,6 +60,7 @@ uint64_t oracle_draw(uint64_t seed, uint32_t tag, uint32_t qid, uint32_t t, uint
 
 #define TAG_POS 1u
 #define TAG_NEG 2u
+#define TAG_SHARED 3u   /* the candidate set shared by a minibatch */
 
 /* ------------------------------------------------------------------- graph */
 /* The KG is a set of triples (Sec. 2); A_r(v) is the set of tails of v under
@@ -543,6 +544,28 @@ static int hset_insert(hset *h, int32_t x)   /* 1 if newly inserted */
     return 1;
 }
 
+/* Positive of query id qid: the first accepted attempt of reverse
+   directional sampling (root uniform over entities with an in-edge, then
+   the walk).  Returns 1 with the grounding in *w, the root in *root and the
+   attempts used in *attempts; 0 when all pos_tries attempts are rejected. */
+static int sample_positive(const okg *g, const otype *T, const oracle_args *a, uint32_t qid,
+                           walk *w, int32_t *root, int32_t *attempts)
+{
+    for (uint32_t t = 0; t < (uint32_t)a->pos_tries; t++) {
+        w->g = g; w->seed = a->seed; w->qid = qid; w->t = t; w->j = 1; w->max_fanout = a->max_fanout;
+        for (int k = 0; k < 3; k++) { w->anchors[k] = -1; w->relations[k] = -1; }
+        if (g->n_active == 0) continue;
+        uint64_t u = oracle_draw(a->seed, TAG_POS, qid, t, 0);
+        *root = g->active_in[oracle_pick(u, (uint64_t)g->n_active)];
+        if (ground(w, T, T->root, *root)) {
+            *attempts = (int32_t)t + 1;
+            return 1;
+        }
+    }
+    *attempts = a->pos_tries;
+    return 0;
+}
+
 static void sample_one(const okg *g, const otype *T, const oracle_args *a, int64_t b,
                        int32_t *anchors, int32_t *relations, int32_t *positive, int32_t *negatives,
                        int32_t *n_valid, int32_t *pos_attempts, int32_t *neg_draws)
@@ -551,26 +574,13 @@ static void sample_one(const okg *g, const otype *T, const oracle_args *a, int64
     for (int k = 0; k < 3; k++) { anchors[3 * b + k] = -1; relations[3 * b + k] = -1; }
     for (int k = 0; k < a->n_neg; k++) negatives[(int64_t)a->n_neg * b + k] = -1;
     positive[b] = -1;
-    /* positive: first accepted attempt */
-    int found = 0;
     walk w;
     int32_t root = -1;
-    uint32_t t;
-    for (t = 0; t < (uint32_t)a->pos_tries && !found; t++) {
-        w.g = g; w.seed = a->seed; w.qid = qid; w.t = t; w.j = 1; w.max_fanout = a->max_fanout;
-        for (int k = 0; k < 3; k++) { w.anchors[k] = -1; w.relations[k] = -1; }
-        if (g->n_active == 0) continue;
-        uint64_t u = oracle_draw(a->seed, TAG_POS, qid, t, 0);
-        root = g->active_in[oracle_pick(u, (uint64_t)g->n_active)];
-        found = ground(&w, T, T->root, root);
-    }
-    if (!found) {
+    if (!sample_positive(g, T, a, qid, &w, &root, &pos_attempts[b])) {
         n_valid[b] = -1;
-        pos_attempts[b] = a->pos_tries;
         neg_draws[b] = -1;
         return;
     }
-    pos_attempts[b] = (int32_t)t;   /* t was incremented past the accepted attempt */
     positive[b] = root;
     for (int k = 0; k < 3; k++) { anchors[3 * b + k] = w.anchors[k]; relations[3 * b + k] = w.relations[k]; }
     /* negatives: rejection sampling against the full answer set */
@@ -610,6 +620,65 @@ int oracle_sample(const okg *g, int qtype, const oracle_args *a, int32_t *anchor
     for (int64_t b = 0; b < a->batch; b++)
         sample_one(g, T, a, b, anchors, relations, positive, negatives, n_valid, pos_attempts,
                    neg_draws);
+    return 0;
+}
+
+/* ------------------------------------------------------ shared negatives */
+/* Sharing negative samples within a minibatch (Sec. 4.3): one candidate set
+   N for all queries and Mask[i][k] = 1 iff N[k] is a negative of query i,
+   i.e. not in its answer set.  N holds the first n_neg distinct values of
+   the draws c_j = pick(U(SHARED, qid0, 0, j), V), j < neg_tries, with qid0
+   the minibatch's query_offset; the positives are those of oracle_sample. */
+int oracle_sample_shared(const okg *g, int qtype, const oracle_args *a, int32_t *anchors,
+                         int32_t *relations, int32_t *positive, int32_t *pos_attempts,
+                         int32_t *shared, int32_t *n_shared, uint32_t *mask, int32_t *n_valid,
+                         int nthreads)
+{
+    if (!g || !a || qtype < 0 || qtype > 8) return -1;
+    if (a->batch < 0 || a->n_neg < 0 || a->pos_tries < 1 || a->neg_tries < a->n_neg) return -1;
+    if (a->query_offset + (uint64_t)a->batch > (1ULL << 32)) return -1;
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+    const otype *T = &TYPES[qtype];
+    /* the shared candidate set */
+    uint32_t cap = 16;
+    while (cap < 2u * (uint32_t)a->neg_tries) cap <<= 1;
+    hset seen = {(int32_t *)malloc((size_t)cap * 4), cap - 1};
+    memset(seen.slot, 0xFF, (size_t)cap * 4);
+    int32_t cnt = 0;
+    for (int32_t j = 0; j < a->neg_tries && cnt < a->n_neg; j++) {
+        uint64_t u = oracle_draw(a->seed, TAG_SHARED, (uint32_t)a->query_offset, 0, (uint32_t)j);
+        int32_t c = (int32_t)oracle_pick(u, (uint64_t)g->V);
+        if (hset_insert(&seen, c)) shared[cnt++] = c;
+    }
+    free(seen.slot);
+    for (int32_t k = cnt; k < a->n_neg; k++) shared[k] = -1;
+    *n_shared = cnt;
+    const int64_t words = (a->n_neg + 31) / 32;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+    for (int64_t b = 0; b < a->batch; b++) {
+        uint32_t qid = (uint32_t)(a->query_offset + (uint64_t)b);
+        uint32_t *row = mask + words * b;
+        for (int64_t w = 0; w < words; w++) row[w] = 0;
+        for (int k = 0; k < 3; k++) { anchors[3 * b + k] = -1; relations[3 * b + k] = -1; }
+        positive[b] = -1;
+        walk w;
+        int32_t root = -1;
+        if (!sample_positive(g, T, a, qid, &w, &root, &pos_attempts[b])) {
+            n_valid[b] = -1;
+            continue;
+        }
+        positive[b] = root;
+        for (int k = 0; k < 3; k++) { anchors[3 * b + k] = w.anchors[k]; relations[3 * b + k] = w.relations[k]; }
+        iset Aq = eval_node(g, T, T->root, w.anchors, w.relations);
+        int32_t kept = 0;
+        for (int32_t k = 0; k < cnt; k++)
+            if (!set_has(Aq, shared[k])) {
+                row[k / 32] |= 1u << (k % 32);
+                kept++;
+            }
+        n_valid[b] = kept;
+        free(Aq.v);
+    }
     return 0;
 }
 

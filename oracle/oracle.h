@@ -71,6 +71,18 @@ int oracle_sample(const okg *g, int qtype, const oracle_args *a, int32_t *anchor
                   int32_t *relations, int32_t *positive, int32_t *negatives, int32_t *n_valid,
                   int32_t *pos_attempts, int32_t *neg_draws, int nthreads);
 
+/* Shared negatives of a minibatch (Sec. 4.3): positives as oracle_sample;
+   shared [n_neg] = the first n_neg distinct values of the draws
+   pick(U(3, query_offset, 0, j), V), j < neg_tries, in draw order, -1 padded,
+   *n_shared = their number; mask [batch * ceil(n_neg / 32)] bit k % 32 of
+   word k / 32 of row i set iff shared[k] is not an answer of query i;
+   n_valid [batch] = set bits of the row, -1 for a query without a positive.
+   Returns 0, or -1 on invalid arguments. */
+int oracle_sample_shared(const okg *g, int qtype, const oracle_args *a, int32_t *anchors,
+                         int32_t *relations, int32_t *positive, int32_t *pos_attempts,
+                         int32_t *shared, int32_t *n_shared, uint32_t *mask, int32_t *n_valid,
+                         int nthreads);
+
 /* Exhaustive answer set of a grounded query; writes up to cap sorted ids to
    out and returns |A_q| (or -1 on bad input). */
 int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
