@@ -157,6 +157,41 @@ def c_sweep(cfg, triples, g, threads, stream, seconds):
     del og
 
 
+def shared_bench(cfg, g, types, steps, warmup, stream):
+    """Shared-negative minibatches (Sec. 4.3, sharing negative samples): the
+    workload's batch of queries shares one set of n_neg candidates and gets a
+    mask of verified negatives.  Prints one JSON line per shape with the
+    minibatch time and the (query, candidate) pairs verified per second."""
+    import numpy as np
+    import torch
+
+    import paper_2110_14890_amd as sm
+
+    for qt in types:
+        dag = sm.query_preset(qt)
+        args = sm.make_args(cfg.batch, cfg.n_neg, seed=cfg.seed, neg_tries=4 * cfg.n_neg)
+        out = sm.alloc_shared_outputs(cfg.batch, cfg.n_neg)
+        for _ in range(warmup):
+            sm.sample_shared_into(g, dag, args, out, stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            sm.sample_shared_into(g, dag, args, out, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        nv = out["n_valid"].cpu().numpy()
+        ns = int(out["n_shared"].item())
+        valid = int((nv >= 0).sum())
+        print(json.dumps({"mode": "shared_negatives", "shape": qt, "queries": cfg.batch,
+                          "shared_candidates": ns, "ms_per_minibatch": round(ms, 4),
+                          "queries_per_s": round(cfg.batch / (ms / 1e3), 1),
+                          "pairs_per_s": round(valid * ns / (ms / 1e3), 1),
+                          "mean_negatives_per_query": round(float(nv[nv >= 0].mean()), 2)}),
+              flush=True)
+
+
 def cpu_baseline(cfg, triples, types, seconds, threads):
     """The CPU oracle, timed on the host on the first queries of each shape
     (a bounded sample of the same workload)."""
@@ -199,6 +234,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-ceiling", action="store_true")
+    ap.add_argument("--shared", action="store_true",
+                    help="instead of the benchmark: minibatches sharing one candidate set")
     ap.add_argument("--c-sweep", action="store_true",
                     help="instead of the benchmark: minibatch time vs max expansion C, "
                          "GPU vs the exhaustive CPU oracle (2p, ip)")
@@ -250,6 +287,9 @@ def main():
     stream = torch.cuda.current_stream()
     if args.c_sweep:
         c_sweep(cfg, triples, g, threads, stream, args.cpu_seconds)
+        return
+    if args.shared:
+        shared_bench(cfg, g, types, args.steps, args.warmup, stream)
         return
     neg_tries = 4 * cfg.n_neg
     dags = {qt: sm.query_preset(qt) for qt in types}

@@ -188,6 +188,38 @@ int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
                            int64_t *stats, void *workspace, size_t ws_bytes, void *hip_stream);
 
+/* Caller-owned device outputs of smore_sample_shared, int32 unless noted.
+   anchors [B,3], relations [B,3], positive [B], pos_attempts [B]
+                     as in smore_sample_out
+   shared   [n_neg]  the minibatch's candidate set N, in draw order, -1 padded
+   n_shared [1]      |N|: n_neg, or fewer when neg_tries draws hold fewer
+                     distinct entities
+   mask     uint32 [B, (n_neg + 31) / 32]: bit k % 32 of word k / 32 of row i
+                     is set iff N[k] is a verified non-answer of query i
+   n_valid  [B]      set bits of row i; -1 for a query without a positive
+                     (its row is zero)
+   All pointers are required (shared and mask may be NULL when n_neg = 0). */
+typedef struct {
+    int32_t *anchors, *relations, *positive, *pos_attempts, *shared, *n_shared;
+    uint32_t *mask;
+    int32_t *n_valid;
+} smore_shared_out;
+
+/* A minibatch whose queries share one set of candidate negatives (Sec. 4.3,
+   sharing negative samples): one candidate set N for all args->batch
+   queries and a mask saying, per query, which members of N are negatives.
+   The positives are exactly those of smore_sample with the same arguments.
+   N holds the first n_neg distinct values of the draws
+   pick(U(3, query_offset, 0, j), V), j < neg_tries (Philox counter
+   (j, 0, low 32 bits of query_offset, 3)), so different minibatches
+   (query_offset) draw different sets.  Every (query, member) pair is
+   verified by the same bidirectional test as smore_sample.  Arguments,
+   validation and workspace (smore_sample_workspace_bytes with the same
+   args) as for smore_sample; asynchronous on hip_stream. */
+int smore_sample_shared(const smore_graph *g, const smore_query_dag *dag,
+                        const smore_sample_args *args, const smore_shared_out *out,
+                        void *workspace, size_t ws_bytes, void *hip_stream);
+
 /* Instrumentation: the next smore_sample or smore_sample_negatives call
    made by this thread records the caller's HIP events (hipEvent_t) on its
    stream immediately before and after one of its kernels in the first

@@ -45,6 +45,14 @@ class SampleOut(ctypes.Structure):
                                     "pos_attempts", "neg_draws")]
 
 
+SHARED_FIELDS = ("anchors", "relations", "positive", "pos_attempts", "shared", "n_shared", "mask",
+                 "n_valid")
+
+
+class SharedOut(ctypes.Structure):
+    _fields_ = [(n, c_vp) for n in SHARED_FIELDS]
+
+
 OUT_FIELDS = ("anchors", "relations", "positive", "negatives", "n_valid", "pos_attempts",
               "neg_draws")
 
@@ -77,6 +85,8 @@ def lib() -> ctypes.CDLL:
                                                    ctypes.POINTER(ctypes.c_size_t)]
         L.smore_sample.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
                                    ctypes.POINTER(SampleOut), c_vp, ctypes.c_size_t, c_vp]
+        L.smore_sample_shared.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
+                                          ctypes.POINTER(SharedOut), c_vp, ctypes.c_size_t, c_vp]
         L.smore_sample_positives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp]
@@ -215,6 +225,38 @@ def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream
     _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                               ctypes.byref(_out_struct(out)), wp, wn, _stream_handle(stream)))
     return out
+
+
+def alloc_shared_outputs(batch: int, n_shared: int, device=None) -> dict:
+    """Device outputs of sample_shared_into (the mask is int32 storage of the
+    uint32 words)."""
+    import torch
+    dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
+    z = lambda *s: torch.empty(s, dtype=torch.int32, device=dev)
+    return {"anchors": z(batch, 3), "relations": z(batch, 3), "positive": z(batch),
+            "pos_attempts": z(batch), "shared": z(n_shared), "n_shared": z(1),
+            "mask": z(batch, (n_shared + 31) // 32), "n_valid": z(batch)}
+
+
+def sample_shared_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
+                       workspace: "Workspace | None" = None) -> dict:
+    """smore_sample_shared: args.n_neg is the size of the shared candidate set."""
+    wp, wn = _workspace(workspace, dag, args)
+    st = SharedOut(*[out[k].data_ptr() if out[k].numel() else None for k in SHARED_FIELDS])
+    _check(lib().smore_sample_shared(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                     ctypes.byref(st), wp, wn, _stream_handle(stream)))
+    return out
+
+
+def sample_shared(graph: Graph, qtype: "str | QueryDag", batch: int, n_shared: int, seed: int = 0,
+                  query_offset: int = 0, pos_tries: int = 64, neg_tries: int | None = None,
+                  max_fanout: int = 0, stream=None) -> dict:
+    """A minibatch of `batch` queries sharing one set of `n_shared` candidate
+    negatives, with the mask of verified negatives per query."""
+    dag = query_preset(qtype) if isinstance(qtype, str) else qtype
+    args = make_args(batch, n_shared, seed, query_offset, pos_tries, neg_tries, max_fanout)
+    out = alloc_shared_outputs(batch, n_shared)
+    return sample_shared_into(graph, dag, args, out, stream)
 
 
 def _out_struct(out: dict) -> SampleOut:

@@ -387,13 +387,10 @@ namespace {
 
 enum Stage { POS = 1, NEG = 2 };
 
-// Validation shared by the sampling entry points, then the launch(es).
-int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
-               const smore_sample_out* out, int64_t* stats, void* workspace, size_t ws_bytes,
-               void* hip_stream, int stages)
+// Checks of the plan and the arguments common to the sampling entry points
+// (host only); *qt receives the shape.
+int check_args(const smore_query_dag* dag, const smore_sample_args* a, int* qt_out)
 {
-    // host-side checks first (they need no device), the graph last
-    if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
     int rc = check_dag(dag);
     if (rc) return rc;
     for (int k = 0; k < dag->n_nodes; ++k)
@@ -415,17 +412,19 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
     if (a->flags != 0) return fail(SMORE_E_INVALID_ARG, "flags must be 0");
     if (a->query_offset > (1ull << 32) || a->query_offset + (uint64_t)a->batch > (1ull << 32))
         return fail(SMORE_E_OVERFLOW, "query ids must stay below 2^32");
-    if (!out->anchors || !out->relations || !out->positive || !out->n_valid ||
-        ((stages & POS) && !out->pos_attempts) || ((stages & NEG) && !out->neg_draws) ||
-        ((stages & NEG) && a->n_neg > 0 && !out->negatives))
-        return fail(SMORE_E_INVALID_ARG, "an output pointer is NULL");
+    *qt_out = qt;
+    return SMORE_OK;
+}
+
+// The graph's device is the current one, and the planner's cut for the
+// shape is the one the kernels implement.
+int check_graph_and_cut(const smore_graph* g, const smore_query_dag* dag, int qt)
+{
     if (!g) return fail(SMORE_E_INVALID_ARG, "graph is NULL");
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return fail(SMORE_E_HIP, "hipGetDevice failed");
     if (dev != g->device)
         return fail(SMORE_E_INVALID_ARG, "graph lives on device %d, current device is %d", g->device, dev);
-
-    // the kernels are written for the cut the planner picks with tie_break 0
     Planner P;
     P.d = dag;
     P.tie = 0;
@@ -433,7 +432,11 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
     bool match = P.n_cut == kKernelCut[qt][0];
     for (int k = 0; match && k < P.n_cut; ++k) match = P.cut[k] == kKernelCut[qt][k + 1];
     if (!match) return fail(SMORE_E_UNSUPPORTED, "internal: planner cut differs from the kernel's");
+    return SMORE_OK;
+}
 
+smore::SampleParams params_of(const smore_sample_args* a)
+{
     smore::SampleParams p;
     p.batch = a->batch;
     p.n_neg = a->n_neg;
@@ -442,6 +445,25 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
     p.max_fanout = a->max_fanout;
     p.seed = a->seed;
     p.query_offset = a->query_offset;
+    return p;
+}
+
+// Validation shared by the sampling entry points, then the launch(es).
+int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
+               const smore_sample_out* out, int64_t* stats, void* workspace, size_t ws_bytes,
+               void* hip_stream, int stages)
+{
+    // host-side checks first (they need no device), the graph last
+    if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
+    int qt = -1;
+    int rc = check_args(dag, a, &qt);
+    if (rc) return rc;
+    if (!out->anchors || !out->relations || !out->positive || !out->n_valid ||
+        ((stages & POS) && !out->pos_attempts) || ((stages & NEG) && !out->neg_draws) ||
+        ((stages & NEG) && a->n_neg > 0 && !out->negatives))
+        return fail(SMORE_E_INVALID_ARG, "an output pointer is NULL");
+    if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
+    const smore::SampleParams p = params_of(a);
     const char* err = "";
     if (stages & POS) {
         smore::WalkProgram w;
@@ -469,6 +491,42 @@ int smore_sample(const smore_graph* g, const smore_query_dag* dag, const smore_s
                  const smore_sample_out* out, void* workspace, size_t ws_bytes, void* hip_stream)
 {
     return run_sample(g, dag, a, out, nullptr, workspace, ws_bytes, hip_stream, POS | NEG);
+}
+
+int smore_sample_shared(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
+                        const smore_shared_out* out, void* workspace, size_t ws_bytes,
+                        void* hip_stream)
+{
+    if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
+    int qt = -1;
+    int rc = check_args(dag, a, &qt);
+    if (rc) return rc;
+    if (!out->anchors || !out->relations || !out->positive || !out->pos_attempts ||
+        !out->n_shared || !out->n_valid || (a->n_neg > 0 && (!out->mask || !out->shared)))
+        return fail(SMORE_E_INVALID_ARG, "an output pointer is NULL");
+    if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
+    const smore::SampleParams p = params_of(a);
+    if (!workspace || ws_bytes < smore::negatives_workspace_bytes(p))
+        return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
+                    smore::negatives_workspace_bytes(p));
+    // positives exactly as smore_sample (same draws), into the shared outputs
+    smore_sample_out pos;
+    std::memset(&pos, 0, sizeof(pos));
+    pos.anchors = out->anchors;
+    pos.relations = out->relations;
+    pos.positive = out->positive;
+    pos.pos_attempts = out->pos_attempts;
+    pos.n_valid = out->n_valid;
+    smore::WalkProgram w;
+    std::memset(&w, 0, sizeof(w));
+    compile_walk(dag, dag->root, 0, &w);
+    const char* err = "";
+    rc = smore::launch_positive(g, w, p, pos, (hipStream_t)hip_stream, &err);
+    if (rc) return fail(rc, "positive sampling: %s", err);
+    rc = smore::launch_shared(g, (smore::QType)qt, p, pos, out->shared, out->n_shared, out->mask,
+                              workspace, ws_bytes, (hipStream_t)hip_stream, &err);
+    if (rc) return fail(rc, "shared negatives: %s", err);
+    return ok();
 }
 
 int smore_sample_positives(const smore_graph* g, const smore_query_dag* dag,

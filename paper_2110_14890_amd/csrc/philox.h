@@ -11,7 +11,7 @@
 
 namespace smore {
 
-enum : uint32_t { TAG_POS = 1u, TAG_NEG = 2u };
+enum : uint32_t { TAG_POS = 1u, TAG_NEG = 2u, TAG_SHARED = 3u };
 
 struct U4 {
     uint32_t x, y, z, w;

@@ -797,15 +797,17 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     if (stats)
         for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
     if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
-        for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
+        if (!p.shared_mode) {   // a shared-candidate minibatch has no per-query rows
+            for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
+            out.neg_draws[b] = -1;
+        }
         out.n_valid[b] = -1;
-        out.neg_draws[b] = -1;
         q[6] = -1;   // skipped by the rounds
         return;
     }
     if (p.n_neg == 0) {
         out.n_valid[b] = 0;
-        out.neg_draws[b] = 0;
+        if (!p.shared_mode) out.neg_draws[b] = 0;
         return;
     }
     T tl;
@@ -847,11 +849,14 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int QT, class T>
+// SH: the candidates are the minibatch's shared set p.shared (j < its
+// size) instead of the query's own draws.
+template <int QT, class T, bool SH = false>
 __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p, smore_sample_out out,
                                                     Ws ws, int64_t* stats, int cur, int32_t j0,
                                                     int32_t j1)
 {
+    if constexpr (SH) j1 = min(j1, uni(*p.n_shared));
     __shared__ int32_t stage_all[CWG / 64][STAGE];
     __shared__ int32_t sc_all[CWG / 64][WIN];
     __shared__ uint16_t sj_all[CWG / 64][WIN];
@@ -906,7 +911,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 c[k] = 0;
                 word[k] = 0;
                 if (j < j1) {
-                    c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)g.V);
+                    if constexpr (SH)
+                        c[k] = p.shared[j];
+                    else
+                        c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j),
+                                                     (uint32_t)g.V);
                     if (!use_lists) word[k] = g.has_in[c[k] >> 5];
                 }
             }
@@ -1329,6 +1338,115 @@ int dispatch_negatives(QType qt, const GraphView& gv, const SampleParams& p, con
     }
 }
 
+// ------------------------------------------------- shared candidate sets
+// The minibatch's candidate set: the first n_neg distinct values of the
+// draws j < neg_tries of the shared stream, in draw order.  One workgroup
+// takes the draws 256 at a time; an LDS table of (value, first draw)
+// decides first occurrences (later blocks find the values of earlier ones).
+constexpr int SSET_WG = 256;
+
+__global__ __launch_bounds__(SSET_WG) void k_shared_set(SampleParams p, int32_t V, int32_t* shared,
+                                                        int32_t* n_shared, int32_t tcap, int tshift)
+{
+    extern __shared__ int32_t lds[];   // tv[tcap], tj[tcap], wave_cnt[4]: all dynamic
+    int32_t* tv = lds;
+    int32_t* tj = lds + tcap;
+    int32_t* wave_cnt = lds + 2 * tcap;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const uint32_t tmask = (uint32_t)tcap - 1;
+    for (int32_t k = tid; k < tcap; k += SSET_WG) { tv[k] = -1; tj[k] = INT_MAX; }
+    __syncthreads();
+    int32_t acc = 0;   // the same in every thread: block-wide counts only
+    for (int32_t base = 0; base < p.neg_tries && acc < p.n_neg; base += SSET_WG) {
+        const int32_t j = base + tid;
+        int32_t c = -1;
+        if (j < p.neg_tries) {
+            c = (int32_t)reduce_range(draw64(p.seed, TAG_SHARED, (uint32_t)p.query_offset, 0, (uint32_t)j),
+                                      (uint32_t)V);
+            ht_insert(tv, tj, tmask, tshift, c, j);
+        }
+        __syncthreads();
+        const bool first = c >= 0 && ht_first(tv, tj, tmask, tshift, c) == j;
+        const uint64_t m = __ballot(first);
+        if (lane == 0) wave_cnt[w] = __popcll(m);
+        __syncthreads();
+        int32_t before = 0, total = 0;
+        for (int k = 0; k < SSET_WG / 64; ++k) {
+            before += k < w ? wave_cnt[k] : 0;
+            total += wave_cnt[k];
+        }
+        const int32_t rank = acc + before + __popcll(m & lanes_below(lane));
+        if (first && rank < p.n_neg) shared[rank] = c;
+        acc = min(p.n_neg, acc + total);
+        __syncthreads();   // wave_cnt is rewritten by the next block of draws
+    }
+    for (int32_t k = acc + tid; k < p.n_neg; k += SSET_WG) shared[k] = -1;
+    if (tid == 0) *n_shared = acc;
+}
+
+// Mask rows from the pair states: bit k of row b set iff state (b, k) is a
+// non-answer; n_valid = set bits.  One wavefront per query.
+__global__ __launch_bounds__(256) void k_pack(SampleParams p, Ws ws, uint32_t* mask, int32_t* n_valid)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t words = (p.n_neg + 31) >> 5;
+    const int32_t ns = uni(*p.n_shared);
+    const int32_t nwaves = gridDim.x * 4;
+    for (int32_t b = uni(blockIdx.x * 4 + (threadIdx.x >> 6)); b < p.batch; b += nwaves) {
+        uint32_t* row = mask + (int64_t)b * words;
+        const bool valid = uni(ws.qf[(int64_t)b * QF + 6]) >= 0;
+        const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
+        int32_t cnt = 0;
+        for (int32_t wd = lane; wd < words; wd += 64) {
+            uint32_t bits = 0;
+            if (valid)
+                for (int k = 0; k < 32; ++k) {
+                    const int32_t j = wd * 32 + k;
+                    if (j < ns && sv[j] == ST_NON) bits |= 1u << k;
+                }
+            row[wd] = bits;
+            cnt += __popc(bits);
+        }
+        for (int s = 32; s > 0; s >>= 1) cnt += __shfl_xor(cnt, s);
+        if (valid && lane == 0) n_valid[b] = cnt;
+    }
+}
+
+template <int QT>
+int run_shared(const GraphView& gv, const SampleParams& p, const smore_sample_out& pos, Ws ws,
+               int32_t* shared, int32_t* n_shared, uint32_t* mask, int32_t R, hipStream_t st,
+               const char** err)
+{
+    int rc;
+    const int32_t tcap = compact_tcap(p.neg_tries > 0 ? p.neg_tries : 1);
+    int tshift = 32;
+    for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
+    // the table needs up to 64 KiB plus the counts: raise the kernel's LDS
+    // limit to the largest request once (the default is 64 KiB in total)
+    const size_t lds = ((size_t)2 * tcap + SSET_WG / 64) * sizeof(int32_t);
+    static bool attr = false;
+    if (!attr) {
+        const size_t most = ((size_t)2 * compact_tcap(SMORE_MAX_NEG_TRIES) + SSET_WG / 64) * sizeof(int32_t);
+        const hipError_t e = hipFuncSetAttribute((const void*)k_shared_set,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)most);
+        if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
+        attr = true;
+    }
+    k_shared_set<<<1, SSET_WG, lds, st>>>(p, gv.V, shared, n_shared, tcap, tshift);
+    if ((rc = check_launch(err))) return rc;
+    k_prepare<QT, NoTally><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, pos, ws, nullptr, R);
+    if ((rc = check_launch(err))) return rc;
+    if (p.n_neg == 0) return SMORE_OK;
+    k_candidates<QT, NoTally, true><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, pos, ws, nullptr, 0, 0,
+                                                                    p.n_neg);
+    if ((rc = check_launch(err))) return rc;
+    k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, pos, ws, nullptr, 1);
+    if ((rc = check_launch(err))) return rc;
+    k_pack<<<(p.batch + 3) / 4 < PERSIST_BLOCKS ? (p.batch + 3) / 4 : PERSIST_BLOCKS, 256, 0, st>>>(
+        p, ws, mask, pos.n_valid);
+    return check_launch(err);
+}
+
 GraphView view_of(const smore_graph* g)
 {
     GraphView gv;
@@ -1379,6 +1497,35 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
                          : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
     g_prof = ProfileArm{};  // one-shot: an arm never outlives the call it was meant for
     return rc;
+}
+
+int launch_shared(const smore_graph* g, QType qt, const SampleParams& p0, const smore_sample_out& pos,
+                  int32_t* shared, int32_t* n_shared, uint32_t* mask, void* workspace,
+                  size_t ws_bytes, hipStream_t st, const char** err)
+{
+    SampleParams p = p0;
+    p.shared_mode = 1;
+    p.shared = shared;
+    p.n_shared = n_shared;
+    Ws ws;
+    const size_t need = ws_layout(p, &ws, (char*)workspace);
+    if (!workspace || ws_bytes < need) {
+        *err = "workspace too small (see smore_sample_workspace_bytes)";
+        return SMORE_E_INVALID_ARG;
+    }
+    const GraphView gv = view_of(g);
+    switch (qt) {
+        case Q1P: return run_shared<Q1P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case Q2P: return run_shared<Q2P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case Q3P: return run_shared<Q3P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case Q2I: return run_shared<Q2I>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case Q3I: return run_shared<Q3I>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case QIP: return run_shared<QIP>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case QPI: return run_shared<QPI>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case Q2U: return run_shared<Q2U>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        case QUP: return run_shared<QUP>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
+        default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
+    }
 }
 
 }  // namespace smore

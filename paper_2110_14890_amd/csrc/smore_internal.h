@@ -51,6 +51,12 @@ enum QType { Q1P = 0, Q2P, Q3P, Q2I, Q3I, QIP, QPI, Q2U, QUP, NQTYPE };
 struct SampleParams {
     int32_t batch, n_neg, pos_tries, neg_tries, max_fanout;
     uint64_t seed, query_offset;
+    // shared-candidate minibatches (shared_mode 1): the candidate set and its
+    // size (device; the set is NULL when it is empty); per-query negatives
+    // have shared_mode 0 and write per-query rows and draw counts instead
+    int32_t shared_mode = 0;
+    const int32_t* shared = nullptr;
+    const int32_t* n_shared = nullptr;
 };
 
 }  // namespace smore
@@ -75,6 +81,9 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
                     const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
                     hipStream_t stream, const char** err);
 size_t negatives_workspace_bytes(const SampleParams& p);
+int launch_shared(const smore_graph* g, QType qt, const SampleParams& p, const smore_sample_out& pos,
+                  int32_t* shared, int32_t* n_shared, uint32_t* mask, void* workspace,
+                  size_t ws_bytes, hipStream_t stream, const char** err);
 // one-shot event pair recorded around one kernel of the next negatives call
 void arm_profile(void* start_event, void* stop_event, int which);
 int64_t gather_probe_threads(int64_t n_reads);

@@ -234,3 +234,28 @@ def test_gather_probe_validation_on_host(L):
     assert L.smore_gather_probe(fake, 1 << 20, 0, fake, 1, None) == -1       # no reads
     assert L.smore_gather_probe(fake, 1 << 20, 6400, fake, 99, None) == -1   # sink needs 100 words
     assert b"sink" in L.smore_last_error()
+
+
+def test_shared_sample_validation_on_host(L):
+    dag = sm.query_preset("2p")
+    args = sm.make_args(8, 4)
+    vp = ctypes.c_void_p
+    fake = vp(0x1000)
+    full = sm.SharedOut(*([fake] * 8))
+    # NULL out, a missing required pointer, a missing mask when n_neg > 0
+    assert L.smore_sample_shared(None, ctypes.byref(dag), ctypes.byref(args), None, fake, 1 << 20,
+                                 None) == -1
+    for k in ("anchors", "n_shared", "shared", "mask"):
+        o = sm.SharedOut(*([fake] * 8))
+        setattr(o, k, None)
+        assert L.smore_sample_shared(None, ctypes.byref(dag), ctypes.byref(args), ctypes.byref(o),
+                                     fake, 1 << 20, None) == -1, k
+    # with every pointer the graph is the next thing checked (NULL here)
+    assert L.smore_sample_shared(None, ctypes.byref(dag), ctypes.byref(args), ctypes.byref(full),
+                                 fake, 1 << 20, None) == -1
+    assert b"graph" in L.smore_last_error()
+    # negation is refused before anything else
+    neg = sm.query_preset("2p")
+    neg.node[neg.root].op = 4
+    assert L.smore_sample_shared(None, ctypes.byref(neg), ctypes.byref(args), ctypes.byref(full),
+                                 fake, 1 << 20, None) != 0
