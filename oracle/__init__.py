@@ -73,6 +73,8 @@ def lib():
                                     ctypes.c_int]
         L.oracle_sample_shared.argtypes = [P, ctypes.c_int, ctypes.POINTER(_Args), P, P, P, P, P, P,
                                            P, P, ctypes.c_int]
+        L.oracle_verify.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, P, P, P, P, P,
+                                    ctypes.c_int]
         L.oracle_answer_set.restype = ctypes.c_int64
         L.oracle_answer_set.argtypes = [P, ctypes.c_int, P, P, P, ctypes.c_int64]
         L.oracle_bidir_check.argtypes = [P, ctypes.c_int, P, P, ctypes.c_uint32, ctypes.c_int32, P]
@@ -196,6 +198,20 @@ class Graph:
         if rc != 0:
             raise ValueError("oracle_sample rejected its arguments")
         return out
+
+    def verify(self, qtype: str, anchors, relations, candidates, threads: int = 0):
+        """Mask of the candidates [batch, n] that are entities outside A_q."""
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(relations, np.int32)
+        c = np.ascontiguousarray(candidates, np.int32)
+        batch, n = c.shape
+        mask = np.zeros((batch, (n + 31) // 32), np.uint32)
+        nv = np.zeros(batch, np.int32)
+        rc = lib().oracle_verify(self._h, TYPES.index(qtype), batch, n, a.ctypes.data, r.ctypes.data,
+                                 c.ctypes.data, mask.ctypes.data, nv.ctypes.data, threads)
+        if rc != 0:
+            raise ValueError("oracle_verify rejected its arguments")
+        return {"mask": mask, "n_valid": nv}
 
     def sample_shared(self, qtype: str, batch: int, n_shared: int, seed: int = 0,
                       query_offset: int = 0, pos_tries: int = 64, neg_tries: int | None = None,

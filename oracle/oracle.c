@@ -682,6 +682,52 @@ int oracle_sample_shared(const okg *g, int qtype, const oracle_args *a, int32_t 
     return 0;
 }
 
+/* ------------------------------------------------------------ verification */
+/* Membership of given candidates in the answer sets of given queries (the
+   test a rejection sampler makes, Sec. 3.2; used for evaluation, where the
+   answers of a query differ between nested graphs, appendix on the task
+   setup).  Candidate k of query i is c = candidates[i * n + k]; mask bit k
+   of row i is set iff 0 <= c < V and c is not in A_q; n_valid[i] counts the
+   set bits, or is -1 when an anchor or relation of the query is out of
+   range (its row is zero). */
+int oracle_verify(const okg *g, int qtype, int32_t batch, int32_t n, const int32_t *anchors,
+                  const int32_t *relations, const int32_t *candidates, uint32_t *mask,
+                  int32_t *n_valid, int nthreads)
+{
+    if (!g || qtype < 0 || qtype > 8 || batch < 0 || n < 0) return -1;
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+    const otype *T = &TYPES[qtype];
+    const int64_t words = ((int64_t)n + 31) / 32;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+    for (int64_t i = 0; i < batch; i++) {
+        uint32_t *row = mask + words * i;
+        for (int64_t w = 0; w < words; w++) row[w] = 0;
+        const int32_t *a = anchors + 3 * i, *r = relations + 3 * i;
+        int ok = 1;
+        for (int k = 0; k < T->n; k++) {   /* every slot the plan uses is in range */
+            const onode *nd = &T->nd[k];
+            if (nd->op == N_ANCHOR) ok = ok && a[nd->slot] >= 0 && a[nd->slot] < g->V;
+            if (nd->op == N_PROJ) ok = ok && r[nd->slot] >= 0 && r[nd->slot] < g->R;
+        }
+        if (!ok) {
+            n_valid[i] = -1;
+            continue;
+        }
+        iset Aq = eval_node(g, T, T->root, a, r);
+        int32_t kept = 0;
+        for (int32_t k = 0; k < n; k++) {
+            const int32_t c = candidates[(int64_t)n * i + k];
+            if (c >= 0 && c < g->V && !set_has(Aq, c)) {
+                row[k / 32] |= 1u << (k % 32);
+                kept++;
+            }
+        }
+        n_valid[i] = kept;
+        free(Aq.v);
+    }
+    return 0;
+}
+
 /* --------------------------------------------------- bidirectional check */
 /* Sec. 3.2, bidirectional rejection sampling: the sets at the cut nodes are
    computed from the anchors (forward caching); the candidate is expanded

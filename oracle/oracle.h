@@ -83,6 +83,16 @@ int oracle_sample_shared(const okg *g, int qtype, const oracle_args *a, int32_t 
                          int32_t *shared, int32_t *n_shared, uint32_t *mask, int32_t *n_valid,
                          int nthreads);
 
+/* Membership verification of given candidates: candidates [batch * n];
+   mask [batch * ceil(n / 32)] bit k of row i set iff candidate k of query i
+   is an entity (0 <= c < V) outside the query's answer set; n_valid [batch]
+   = set bits, or -1 when an anchor or relation the shape uses is out of
+   range.  anchors/relations [batch * 3] as in oracle_sample.  Returns 0, or
+   -1 on invalid arguments. */
+int oracle_verify(const okg *g, int qtype, int32_t batch, int32_t n, const int32_t *anchors,
+                  const int32_t *relations, const int32_t *candidates, uint32_t *mask,
+                  int32_t *n_valid, int nthreads);
+
 /* Exhaustive answer set of a grounded query; writes up to cap sorted ids to
    out and returns |A_q| (or -1 on bad input). */
 int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
