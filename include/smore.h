@@ -220,6 +220,28 @@ int smore_sample_shared(const smore_graph *g, const smore_query_dag *dag,
                         const smore_sample_args *args, const smore_shared_out *out,
                         void *workspace, size_t ws_bytes, void *hip_stream);
 
+/* Membership verification of caller-given candidates: for every query i
+   (anchors / relations [B,3], device, as smore_sample writes them) and
+   each of its n = args->n_neg candidates (device int32 [B, n]), is the
+   candidate an entity outside the query's answer set?  This is the test
+   behind rejection sampling (Sec. 3.2, bidirectional), run here on given
+   pairs - for evaluation, where a query's answers differ between nested
+   graphs G_train, G_valid, G_test (appendix on the task setup): verifying
+   the positives of queries sampled on G_test against G_valid finds the
+   answers missing from G_valid.
+   mask  uint32 [B, (n + 31) / 32]: bit k % 32 of word k / 32 of row i set
+         iff candidate k of query i is in [0, V) and not an answer
+   n_valid [B]: set bits of row i; -1 when an anchor or relation the shape
+         uses is out of range (row zero)
+   Candidates outside [0, V) are never negatives and read no graph data.
+   args: batch = B, n_neg = n, neg_tries >= n (workspace sizing as for
+   smore_sample, see smore_sample_workspace_bytes); the other fields are
+   checked as for smore_sample but unused.  Asynchronous on hip_stream. */
+int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_sample_args *args,
+                 const int32_t *anchors, const int32_t *relations, const int32_t *candidates,
+                 uint32_t *mask, int32_t *n_valid, void *workspace, size_t ws_bytes,
+                 void *hip_stream);
+
 /* Instrumentation: the next smore_sample or smore_sample_negatives call
    made by this thread records the caller's HIP events (hipEvent_t) on its
    stream immediately before and after one of its kernels in the first

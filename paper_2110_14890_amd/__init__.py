@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
                                    ctypes.POINTER(SampleOut), c_vp, ctypes.c_size_t, c_vp]
         L.smore_sample_shared.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
                                           ctypes.POINTER(SharedOut), c_vp, ctypes.c_size_t, c_vp]
+        L.smore_verify.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs), c_vp,
+                                   c_vp, c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]
         L.smore_sample_positives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp]
@@ -257,6 +259,27 @@ def sample_shared(graph: Graph, qtype: "str | QueryDag", batch: int, n_shared: i
     args = make_args(batch, n_shared, seed, query_offset, pos_tries, neg_tries, max_fanout)
     out = alloc_shared_outputs(batch, n_shared)
     return sample_shared_into(graph, dag, args, out, stream)
+
+
+def verify(graph: Graph, qtype: "str | QueryDag", anchors, relations, candidates, stream=None,
+           workspace: "Workspace | None" = None) -> dict:
+    """smore_verify: which of the candidates (device int32 [batch, n]) are
+    entities outside each query's answer set.  Returns {"mask" (int32
+    storage of the uint32 words), "n_valid"}."""
+    import torch
+    dag = query_preset(qtype) if isinstance(qtype, str) else qtype
+    batch, n = candidates.shape
+    args = make_args(batch, n, neg_tries=n)
+    dev = candidates.device
+    out = {"mask": torch.empty((batch, (n + 31) // 32), dtype=torch.int32, device=dev),
+           "n_valid": torch.empty(batch, dtype=torch.int32, device=dev)}
+    wp, wn = _workspace(workspace, dag, args)
+    ptr = lambda t: t.data_ptr() if t.numel() else None
+    _check(lib().smore_verify(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                              anchors.data_ptr(), relations.data_ptr(), ptr(candidates),
+                              ptr(out["mask"]), out["n_valid"].data_ptr(), wp, wn,
+                              _stream_handle(stream)))
+    return out
 
 
 def _out_struct(out: dict) -> SampleOut:

@@ -493,6 +493,28 @@ int smore_sample(const smore_graph* g, const smore_query_dag* dag, const smore_s
     return run_sample(g, dag, a, out, nullptr, workspace, ws_bytes, hip_stream, POS | NEG);
 }
 
+int smore_verify(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
+                 const int32_t* anchors, const int32_t* relations, const int32_t* candidates,
+                 uint32_t* mask, int32_t* n_valid, void* workspace, size_t ws_bytes, void* hip_stream)
+{
+    if (!a) return fail(SMORE_E_INVALID_ARG, "args is NULL");
+    int qt = -1;
+    int rc = check_args(dag, a, &qt);
+    if (rc) return rc;
+    if (!anchors || !relations || !n_valid || (a->n_neg > 0 && (!candidates || !mask)))
+        return fail(SMORE_E_INVALID_ARG, "an input or output pointer is NULL");
+    if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
+    const smore::SampleParams p = params_of(a);
+    if (!workspace || ws_bytes < smore::negatives_workspace_bytes(p))
+        return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
+                    smore::negatives_workspace_bytes(p));
+    const char* err = "";
+    rc = smore::launch_verify(g, (smore::QType)qt, p, anchors, relations, candidates, mask, n_valid,
+                              workspace, ws_bytes, (hipStream_t)hip_stream, &err);
+    if (rc) return fail(rc, "verification: %s", err);
+    return ok();
+}
+
 int smore_sample_shared(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
                         const smore_shared_out* out, void* workspace, size_t ws_bytes,
                         void* hip_stream)

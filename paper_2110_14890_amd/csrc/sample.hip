@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <cstring>
 
 #include "philox.h"
 #include "smore_internal.h"
@@ -767,7 +768,7 @@ __device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel
 __device__ __forceinline__ bool query_ok(const GraphView& g, const smore_sample_out& out, int32_t b,
                                          int n_anc, int n_rel, int32_t R, int32_t* anc, int32_t* rel)
 {
-    bool ok = out.positive[b] >= 0;
+    bool ok = !out.positive || out.positive[b] >= 0;   // verification has no positives
     for (int k = 0; k < 3; ++k) {
         rel[k] = out.relations[3 * (int64_t)b + k];
         anc[k] = out.anchors[3 * (int64_t)b + k];
@@ -856,7 +857,8 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                                                     Ws ws, int64_t* stats, int cur, int32_t j0,
                                                     int32_t j1)
 {
-    if constexpr (SH) j1 = min(j1, uni(*p.n_shared));
+    if constexpr (SH)
+        if (p.n_shared) j1 = min(j1, uni(*p.n_shared));
     __shared__ int32_t stage_all[CWG / 64][STAGE];
     __shared__ int32_t sc_all[CWG / 64][WIN];
     __shared__ uint16_t sj_all[CWG / 64][WIN];
@@ -911,17 +913,20 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 c[k] = 0;
                 word[k] = 0;
                 if (j < j1) {
-                    if constexpr (SH)
-                        c[k] = p.shared[j];
-                    else
+                    if constexpr (SH) {
+                        c[k] = p.shared[(int64_t)p.cand_stride * b + j];
+                        if ((uint32_t)c[k] >= (uint32_t)g.V) c[k] = -1;   // never a negative
+                    } else {
                         c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j),
                                                      (uint32_t)g.V);
-                    if (!use_lists) word[k] = g.has_in[c[k] >> 5];
+                    }
+                    if (!use_lists && c[k] >= 0) word[k] = g.has_in[c[k] >> 5];
                 }
             }
             if (use_lists) {
 #pragma unroll
                 for (int k = 0; k < DPW; ++k) {
+                    if (c[k] < 0) continue;   // (candidates given by the caller only)
                     bool hit = !RootLists<QT>::any;
 #pragma unroll
                     for (int f = 0; f < 3; ++f) {
@@ -937,11 +942,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             for (int k = 0; k < DPW; ++k) {
                 const int32_t j = base + k * 64 + lane;
                 const bool live = j < j1;
-                const bool in = live && ((word[k] >> (c[k] & 31)) & 1u);
+                const bool in = live && c[k] >= 0 && ((word[k] >> (c[k] & 31)) & 1u);
                 if (live) {
-                    if (!use_lists) tl.read(g.has_in + (c[k] >> 5), 4);
+                    if (!use_lists && c[k] >= 0) tl.read(g.has_in + (c[k] >> 5), 4);
                     cv[j] = c[k];
-                    if (!in) sv[j] = ST_NON;
+                    if (!in) sv[j] = c[k] >= 0 ? ST_NON : ST_DUP;   // ST_DUP: not an entity
                 }
                 const uint64_t m = __ballot(in);
                 if (in) {
@@ -1390,7 +1395,7 @@ __global__ __launch_bounds__(256) void k_pack(SampleParams p, Ws ws, uint32_t* m
 {
     const int lane = threadIdx.x & 63;
     const int32_t words = (p.n_neg + 31) >> 5;
-    const int32_t ns = uni(*p.n_shared);
+    const int32_t ns = p.n_shared ? uni(*p.n_shared) : p.n_neg;
     const int32_t nwaves = gridDim.x * 4;
     for (int32_t b = uni(blockIdx.x * 4 + (threadIdx.x >> 6)); b < p.batch; b += nwaves) {
         uint32_t* row = mask + (int64_t)b * words;
@@ -1412,12 +1417,10 @@ __global__ __launch_bounds__(256) void k_pack(SampleParams p, Ws ws, uint32_t* m
     }
 }
 
-template <int QT>
-int run_shared(const GraphView& gv, const SampleParams& p, const smore_sample_out& pos, Ws ws,
-               int32_t* shared, int32_t* n_shared, uint32_t* mask, int32_t R, hipStream_t st,
-               const char** err)
+// The minibatch's shared candidate set (one workgroup).
+int draw_shared_set(const SampleParams& p, int32_t V, int32_t* shared, int32_t* n_shared,
+                    hipStream_t st, const char** err)
 {
-    int rc;
     const int32_t tcap = compact_tcap(p.neg_tries > 0 ? p.neg_tries : 1);
     int tshift = 32;
     for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
@@ -1432,19 +1435,45 @@ int run_shared(const GraphView& gv, const SampleParams& p, const smore_sample_ou
         if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
         attr = true;
     }
-    k_shared_set<<<1, SSET_WG, lds, st>>>(p, gv.V, shared, n_shared, tcap, tshift);
-    if ((rc = check_launch(err))) return rc;
-    k_prepare<QT, NoTally><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, pos, ws, nullptr, R);
+    k_shared_set<<<1, SSET_WG, lds, st>>>(p, V, shared, n_shared, tcap, tshift);
+    return check_launch(err);
+}
+
+// Every (query, candidate) pair of p.shared (one set for all queries, or a
+// list per query p.cand_stride apart): states, then mask rows and counts.
+template <int QT>
+int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out& q, Ws ws,
+              uint32_t* mask, int32_t R, hipStream_t st, const char** err)
+{
+    int rc;
+    k_prepare<QT, NoTally><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, q, ws, nullptr, R);
     if ((rc = check_launch(err))) return rc;
     if (p.n_neg == 0) return SMORE_OK;
-    k_candidates<QT, NoTally, true><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, pos, ws, nullptr, 0, 0,
+    k_candidates<QT, NoTally, true><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
                                                                     p.n_neg);
     if ((rc = check_launch(err))) return rc;
-    k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, pos, ws, nullptr, 1);
+    k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
     if ((rc = check_launch(err))) return rc;
     k_pack<<<(p.batch + 3) / 4 < PERSIST_BLOCKS ? (p.batch + 3) / 4 : PERSIST_BLOCKS, 256, 0, st>>>(
-        p, ws, mask, pos.n_valid);
+        p, ws, mask, q.n_valid);
     return check_launch(err);
+}
+
+int dispatch_pairs(QType qt, const GraphView& gv, const SampleParams& p, const smore_sample_out& q,
+                   Ws ws, uint32_t* mask, int32_t R, hipStream_t st, const char** err)
+{
+    switch (qt) {
+        case Q1P: return run_pairs<Q1P>(gv, p, q, ws, mask, R, st, err);
+        case Q2P: return run_pairs<Q2P>(gv, p, q, ws, mask, R, st, err);
+        case Q3P: return run_pairs<Q3P>(gv, p, q, ws, mask, R, st, err);
+        case Q2I: return run_pairs<Q2I>(gv, p, q, ws, mask, R, st, err);
+        case Q3I: return run_pairs<Q3I>(gv, p, q, ws, mask, R, st, err);
+        case QIP: return run_pairs<QIP>(gv, p, q, ws, mask, R, st, err);
+        case QPI: return run_pairs<QPI>(gv, p, q, ws, mask, R, st, err);
+        case Q2U: return run_pairs<Q2U>(gv, p, q, ws, mask, R, st, err);
+        case QUP: return run_pairs<QUP>(gv, p, q, ws, mask, R, st, err);
+        default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
+    }
 }
 
 GraphView view_of(const smore_graph* g)
@@ -1507,6 +1536,7 @@ int launch_shared(const smore_graph* g, QType qt, const SampleParams& p0, const 
     p.shared_mode = 1;
     p.shared = shared;
     p.n_shared = n_shared;
+    p.cand_stride = 0;
     Ws ws;
     const size_t need = ws_layout(p, &ws, (char*)workspace);
     if (!workspace || ws_bytes < need) {
@@ -1514,18 +1544,33 @@ int launch_shared(const smore_graph* g, QType qt, const SampleParams& p0, const 
         return SMORE_E_INVALID_ARG;
     }
     const GraphView gv = view_of(g);
-    switch (qt) {
-        case Q1P: return run_shared<Q1P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case Q2P: return run_shared<Q2P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case Q3P: return run_shared<Q3P>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case Q2I: return run_shared<Q2I>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case Q3I: return run_shared<Q3I>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case QIP: return run_shared<QIP>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case QPI: return run_shared<QPI>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case Q2U: return run_shared<Q2U>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        case QUP: return run_shared<QUP>(gv, p, pos, ws, shared, n_shared, mask, g->R, st, err);
-        default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
+    const int rc = draw_shared_set(p, gv.V, shared, n_shared, st, err);
+    if (rc) return rc;
+    return dispatch_pairs(qt, gv, p, pos, ws, mask, g->R, st, err);
+}
+
+int launch_verify(const smore_graph* g, QType qt, const SampleParams& p0, const int32_t* anchors,
+                  const int32_t* relations, const int32_t* candidates, uint32_t* mask,
+                  int32_t* n_valid, void* workspace, size_t ws_bytes, hipStream_t st,
+                  const char** err)
+{
+    SampleParams p = p0;
+    p.shared_mode = 2;
+    p.shared = candidates;
+    p.n_shared = nullptr;
+    p.cand_stride = p.n_neg;
+    Ws ws;
+    const size_t need = ws_layout(p, &ws, (char*)workspace);
+    if (!workspace || ws_bytes < need) {
+        *err = "workspace too small (see smore_sample_workspace_bytes)";
+        return SMORE_E_INVALID_ARG;
     }
+    smore_sample_out q;
+    std::memset(&q, 0, sizeof(q));
+    q.anchors = (int32_t*)anchors;
+    q.relations = (int32_t*)relations;
+    q.n_valid = n_valid;
+    return dispatch_pairs(qt, view_of(g), p, q, ws, mask, g->R, st, err);
 }
 
 }  // namespace smore

@@ -57,6 +57,10 @@ struct SampleParams {
     int32_t shared_mode = 0;
     const int32_t* shared = nullptr;
     const int32_t* n_shared = nullptr;
+    // candidates of query b start at shared + cand_stride * b (0: one set for
+    // all queries); without n_shared every query has n_neg candidates, and
+    // ids outside [0, V) are never negatives
+    int32_t cand_stride = 0;
 };
 
 }  // namespace smore
@@ -84,6 +88,10 @@ size_t negatives_workspace_bytes(const SampleParams& p);
 int launch_shared(const smore_graph* g, QType qt, const SampleParams& p, const smore_sample_out& pos,
                   int32_t* shared, int32_t* n_shared, uint32_t* mask, void* workspace,
                   size_t ws_bytes, hipStream_t stream, const char** err);
+int launch_verify(const smore_graph* g, QType qt, const SampleParams& p, const int32_t* anchors,
+                  const int32_t* relations, const int32_t* candidates, uint32_t* mask,
+                  int32_t* n_valid, void* workspace, size_t ws_bytes, hipStream_t stream,
+                  const char** err);
 // one-shot event pair recorded around one kernel of the next negatives call
 void arm_profile(void* start_event, void* stop_event, int which);
 int64_t gather_probe_threads(int64_t n_reads);
