@@ -269,6 +269,11 @@ def verify(graph: Graph, qtype: "str | QueryDag", anchors, relations, candidates
     import torch
     dag = query_preset(qtype) if isinstance(qtype, str) else qtype
     batch, n = candidates.shape
+    for name, t, shape in (("anchors", anchors, (batch, 3)), ("relations", relations, (batch, 3)),
+                           ("candidates", candidates, (batch, n))):
+        if tuple(t.shape) != shape or t.dtype != torch.int32 or not t.is_contiguous() \
+                or t.device != candidates.device or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous int32 device tensor of shape {shape}")
     args = make_args(batch, n, neg_tries=n)
     dev = candidates.device
     out = {"mask": torch.empty((batch, (n + 31) // 32), dtype=torch.int32, device=dev),
