@@ -22,7 +22,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "liboracle.so")
-TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
 
 
 def build(force: bool = True) -> str:

@@ -14,7 +14,15 @@
  *     (anchor, relation), or when max_fanout > 0 and a grounded step's
  *     forward neighbour list under its relation exceeds max_fanout;
  *   - candidates are uniform over all V entities, kept iff outside A_q and
- *     not drawn before (the negative set is a set).
+ *     not drawn before (the negative set is a set);
+ *   - a negated operand of an intersection is grounded from a sibling
+ *     entity: the intersection's positive operands are grounded first (from
+ *     the intersection's entity e, in plan order); then one entity w is
+ *     drawn uniformly from A_r(x), where (x, r) -> e is the step of the
+ *     first positive operand; the negated operand's subtree is grounded
+ *     from w by the same reverse walk; the attempt is rejected if e lies in
+ *     the negated operand's set.  The root therefore stays an answer, and
+ *     the negated set overlaps the positive operand's set (it holds w).
  */
 #include "oracle.h"
 
@@ -305,11 +313,13 @@ static void rel_range(const int64_t *off, const int32_t *rel, int32_t v, int32_t
 }
 
 /* ---------------------------------------------------------- query plans */
-/* Computation plans of the nine negation-free structures (Sec. 2, "Query
-   computation plan"; appendix on the computation plan).  Nodes are listed
-   children first.  Projection nodes carry a relation slot, anchors an
-   anchor slot; intersection and union edges carry no relation. */
-enum { N_ANCHOR = 0, N_PROJ = 1, N_AND = 2, N_OR = 3 };
+/* Computation plans of the fourteen query structures of the experiments
+   (Sec. 5.1: the structures of BetaE; the plan operators are those of the
+   appendix on the computation plan): nine without negation and 2in, 3in,
+   inp, pin, pni.  Nodes are listed children first.  Projection nodes carry
+   a relation slot, anchors an anchor slot; intersection, union and
+   complement edges carry no relation. */
+enum { N_ANCHOR = 0, N_PROJ = 1, N_AND = 2, N_OR = 3, N_NOT = 4 };
 typedef struct { int op, nch, ch[3], slot; } onode;
 typedef struct { const char *name; int n, root; onode nd[8]; } otype;
 
@@ -318,8 +328,10 @@ typedef struct { const char *name; int n, root; onode nd[8]; } otype;
 #define AND2(a, b) {N_AND, 2, {a, b, -1}, -1}
 #define AND3(a, b, c) {N_AND, 3, {a, b, c}, -1}
 #define OR2(a, b)  {N_OR, 2, {a, b, -1}, -1}
+#define NOT(c)     {N_NOT, 1, {c, -1, -1}, -1}
+#define NTYPES 14
 
-static const otype TYPES[9] = {
+static const otype TYPES[NTYPES] = {
     {"1p", 2, 1, {A(0), P(0, 0)}},
     {"2p", 3, 2, {A(0), P(0, 0), P(1, 1)}},
     {"3p", 4, 3, {A(0), P(0, 0), P(1, 1), P(2, 2)}},
@@ -329,18 +341,23 @@ static const otype TYPES[9] = {
     {"pi", 6, 5, {A(0), P(0, 0), P(1, 1), A(1), P(3, 2), AND2(2, 4)}},
     {"2u", 5, 4, {A(0), P(0, 0), A(1), P(2, 1), OR2(1, 3)}},
     {"up", 6, 5, {A(0), P(0, 0), A(1), P(2, 1), OR2(1, 3), P(4, 2)}},
+    {"2in", 6, 5, {A(0), P(0, 0), A(1), P(2, 1), NOT(3), AND2(1, 4)}},
+    {"3in", 8, 7, {A(0), P(0, 0), A(1), P(2, 1), A(2), P(4, 2), NOT(5), AND3(1, 3, 6)}},
+    {"inp", 7, 6, {A(0), P(0, 0), A(1), P(2, 1), NOT(3), AND2(1, 4), P(5, 2)}},
+    {"pin", 7, 6, {A(0), P(0, 0), P(1, 1), A(1), P(3, 2), NOT(4), AND2(2, 5)}},
+    {"pni", 7, 6, {A(0), P(0, 0), P(1, 1), NOT(2), A(1), P(4, 2), AND2(3, 5)}},
 };
 
 int oracle_type_id(const char *name)
 {
-    for (int k = 0; k < 9; k++)
+    for (int k = 0; k < NTYPES; k++)
         if (strcmp(TYPES[k].name, name) == 0) return k;
     return -1;
 }
 
 int oracle_type_plan(int qtype, int32_t *op, int32_t *child, int32_t *slot, int32_t *root)
 {
-    if (qtype < 0 || qtype > 8) return -1;
+    if (qtype < 0 || qtype >= NTYPES) return -1;
     const otype *T = &TYPES[qtype];
     for (int k = 0; k < T->n; k++) {
         op[k] = T->nd[k].op;
@@ -419,6 +436,38 @@ static iset set_merge(iset a, iset b, int is_union)
     return o;
 }
 
+/* a minus b for sorted sets (the delayed complement of the appendix on the
+   optimal cut: an intersection with a complemented operand is computed as
+   a set difference instead of materialising the complement). */
+static iset set_minus(iset a, iset b)
+{
+    iset o;
+    o.v = (int32_t *)malloc((size_t)(a.n > 0 ? a.n : 1) * 4);
+    o.n = 0;
+    int64_t j = 0;
+    for (int64_t i = 0; i < a.n; i++) {
+        while (j < b.n && b.v[j] < a.v[i]) j++;
+        if (j < b.n && b.v[j] == a.v[i]) continue;
+        o.v[o.n++] = a.v[i];
+    }
+    return o;
+}
+
+/* V minus s: the complement operator of the appendix on the computation
+   plan, used where a complemented set is not an intersection operand. */
+static iset set_complement(int32_t V, iset s)
+{
+    iset o;
+    o.v = (int32_t *)malloc((size_t)(V - s.n > 0 ? V - s.n : 1) * 4);
+    o.n = 0;
+    int64_t j = 0;
+    for (int32_t x = 0; x < V; x++) {
+        if (j < s.n && s.v[j] == x) { j++; continue; }
+        o.v[o.n++] = x;
+    }
+    return o;
+}
+
 static int set_has(iset s, int32_t x)
 {
     int64_t lo = 0, hi = s.n;
@@ -444,11 +493,34 @@ static iset eval_node(const okg *g, const otype *T, int k, const int32_t *anchor
         iset in = eval_node(g, T, nd->ch[0], anchors, relations);
         out = set_proj(g, in, relations[nd->slot]);
         free(in.v);
+    } else if (nd->op == N_NOT) {
+        iset in = eval_node(g, T, nd->ch[0], anchors, relations);
+        out = set_complement(g->V, in);
+        free(in.v);
     } else {
-        out = eval_node(g, T, nd->ch[0], anchors, relations);
-        for (int c = 1; c < nd->nch; c++) {
+        /* an intersection with at least one positive operand subtracts its
+           complemented operands after intersecting the others */
+        int n_pos = 0;
+        for (int c = 0; c < nd->nch; c++) n_pos += T->nd[nd->ch[c]].op != N_NOT;
+        const int diff = nd->op == N_AND && n_pos > 0;
+        int have = 0;
+        for (int c = 0; c < nd->nch; c++) {
+            if (diff && T->nd[nd->ch[c]].op == N_NOT) continue;
             iset b = eval_node(g, T, nd->ch[c], anchors, relations);
+            if (!have) {
+                out = b;
+                have = 1;
+                continue;
+            }
             iset m = set_merge(out, b, nd->op == N_OR);
+            free(out.v);
+            free(b.v);
+            out = m;
+        }
+        for (int c = 0; diff && c < nd->nch; c++) {
+            if (T->nd[nd->ch[c]].op != N_NOT) continue;
+            iset b = eval_node(g, T, T->nd[nd->ch[c]].ch[0], anchors, relations);
+            iset m = set_minus(out, b);
             free(out.v);
             free(b.v);
             out = m;
@@ -460,7 +532,7 @@ static iset eval_node(const okg *g, const otype *T, int k, const int32_t *anchor
 int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
                           const int32_t *relations, int32_t *out, int64_t cap)
 {
-    if (qtype < 0 || qtype > 8) return -1;
+    if (qtype < 0 || qtype >= NTYPES) return -1;
     const otype *T = &TYPES[qtype];
     for (int k = 0; k < T->n; k++) {
         const onode *nd = &T->nd[k];
@@ -479,19 +551,24 @@ int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
    sampling): depth-first from the root to the anchors, children in index
    order.  A projection node whose output entity is e grounds its relation
    and input entity by g(e): an in-relation of e, then an in-neighbour of e
-   under it.  Intersection and union children take the node's own entity. */
+   under it.  Intersection and union children take the node's own entity;
+   a complemented operand of an intersection is grounded from a sibling
+   entity (reading in the header), after the positive operands. */
 typedef struct {
     const okg *g;
+    const otype *T;
     uint64_t seed;
     uint32_t qid, t, j;
     int32_t max_fanout;
     int32_t anchors[3], relations[3];
+    int32_t ent[8];     /* entity each plan node was grounded with */
 } walk;
 
 static int ground(walk *w, const otype *T, int k, int32_t e)
 {
     const onode *nd = &T->nd[k];
     const okg *g = w->g;
+    w->ent[k] = e;
     if (nd->op == N_ANCHOR) {
         w->anchors[nd->slot] = e;
         return 1;
@@ -514,8 +591,33 @@ static int ground(walk *w, const otype *T, int k, int32_t e)
         w->relations[nd->slot] = r;
         return ground(w, T, nd->ch[0], x);
     }
-    for (int c = 0; c < nd->nch; c++)
+    if (nd->op == N_NOT) return ground(w, T, nd->ch[0], e);
+    int first_pos = -1;
+    for (int c = 0; c < nd->nch; c++) {
+        if (T->nd[nd->ch[c]].op == N_NOT) continue;
+        if (first_pos < 0) first_pos = nd->ch[c];
         if (!ground(w, T, nd->ch[c], e)) return 0;
+    }
+    for (int c = 0; c < nd->nch; c++) {
+        const int neg = nd->ch[c];
+        if (T->nd[neg].op != N_NOT) continue;
+        /* the sibling entity: uniform over A_r(x) of the first positive
+           operand's step (x, r) -> e, which holds e, so it is never empty */
+        const onode *p = &T->nd[first_pos];
+        if (nd->op != N_AND || p->op != N_PROJ) return 0;
+        const int32_t x = w->ent[p->ch[0]], r = w->relations[p->slot];
+        int64_t b, en;
+        rel_range(g->f_off, g->f_rel, x, r, &b, &en);
+        uint64_t u = oracle_draw(w->seed, TAG_POS, w->qid, w->t, w->j);
+        w->j += 1;
+        const int32_t sib = g->f_nbr[b + (int64_t)oracle_pick(u, (uint64_t)(en - b))];
+        if (!ground(w, T, neg, sib)) return 0;
+        /* e must stay outside the complemented set */
+        iset S = eval_node(g, T, T->nd[neg].ch[0], w->anchors, w->relations);
+        const int inside = set_has(S, e);
+        free(S.v);
+        if (inside) return 0;
+    }
     /* two single-projection branches grounded to the same (anchor, relation)
        make a degenerate intersection or union: reject */
     for (int a = 0; a < nd->nch; a++)
@@ -552,7 +654,8 @@ static int sample_positive(const okg *g, const otype *T, const oracle_args *a, u
                            walk *w, int32_t *root, int32_t *attempts)
 {
     for (uint32_t t = 0; t < (uint32_t)a->pos_tries; t++) {
-        w->g = g; w->seed = a->seed; w->qid = qid; w->t = t; w->j = 1; w->max_fanout = a->max_fanout;
+        w->g = g; w->T = T; w->seed = a->seed; w->qid = qid; w->t = t; w->j = 1;
+        w->max_fanout = a->max_fanout;
         for (int k = 0; k < 3; k++) { w->anchors[k] = -1; w->relations[k] = -1; }
         if (g->n_active == 0) continue;
         uint64_t u = oracle_draw(a->seed, TAG_POS, qid, t, 0);
@@ -611,7 +714,7 @@ int oracle_sample(const okg *g, int qtype, const oracle_args *a, int32_t *anchor
                   int32_t *relations, int32_t *positive, int32_t *negatives, int32_t *n_valid,
                   int32_t *pos_attempts, int32_t *neg_draws, int nthreads)
 {
-    if (!g || !a || qtype < 0 || qtype > 8) return -1;
+    if (!g || !a || qtype < 0 || qtype >= NTYPES) return -1;
     if (a->batch < 0 || a->n_neg < 0 || a->pos_tries < 1 || a->neg_tries < a->n_neg) return -1;
     if (a->query_offset + (uint64_t)a->batch > (1ULL << 32)) return -1;
     if (nthreads <= 0) nthreads = omp_get_max_threads();
@@ -634,7 +737,7 @@ int oracle_sample_shared(const okg *g, int qtype, const oracle_args *a, int32_t 
                          int32_t *shared, int32_t *n_shared, uint32_t *mask, int32_t *n_valid,
                          int nthreads)
 {
-    if (!g || !a || qtype < 0 || qtype > 8) return -1;
+    if (!g || !a || qtype < 0 || qtype >= NTYPES) return -1;
     if (a->batch < 0 || a->n_neg < 0 || a->pos_tries < 1 || a->neg_tries < a->n_neg) return -1;
     if (a->query_offset + (uint64_t)a->batch > (1ULL << 32)) return -1;
     if (nthreads <= 0) nthreads = omp_get_max_threads();
@@ -694,7 +797,7 @@ int oracle_verify(const okg *g, int qtype, int32_t batch, int32_t n, const int32
                   const int32_t *relations, const int32_t *candidates, uint32_t *mask,
                   int32_t *n_valid, int nthreads)
 {
-    if (!g || qtype < 0 || qtype > 8 || batch < 0 || n < 0) return -1;
+    if (!g || qtype < 0 || qtype >= NTYPES || batch < 0 || n < 0) return -1;
     if (nthreads <= 0) nthreads = omp_get_max_threads();
     const otype *T = &TYPES[qtype];
     const int64_t words = ((int64_t)n + 31) / 32;
@@ -757,6 +860,7 @@ static int member(bidir *B, int k, int32_t x)
             if (member(B, nd->ch[0], B->g->r_nbr[i])) return 1;
         return 0;
     }
+    if (nd->op == N_NOT) return !member(B, nd->ch[0], x);
     for (int c = 0; c < nd->nch; c++) {
         int in = member(B, nd->ch[c], x);
         if (nd->op == N_AND && !in) return 0;
@@ -785,7 +889,7 @@ static int is_node_cut(const otype *T, uint32_t mask)
 int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const int32_t *relations,
                        uint32_t cut_mask, int32_t c, int64_t *counts)
 {
-    if (qtype < 0 || qtype > 8 || c < 0 || c >= g->V) return -1;
+    if (qtype < 0 || qtype >= NTYPES || c < 0 || c >= g->V) return -1;
     const otype *T = &TYPES[qtype];
     if (!is_node_cut(T, cut_mask)) return -1;
     bidir B;

@@ -56,7 +56,7 @@ int64_t oracle_graph_dump(const okg *g, int dir, int32_t *ent, int32_t *rel, int
 /* Copy active_in (entities with at least one in-edge, ascending). */
 int64_t oracle_graph_active_in(const okg *g, int32_t *out);
 
-/* query types: 0..8 = 1p 2p 3p 2i 3i ip pi 2u up */
+/* query types: 0..13 = 1p 2p 3p 2i 3i ip pi 2u up 2in 3in inp pin pni */
 int oracle_type_id(const char *name);
 
 typedef struct {
@@ -111,7 +111,7 @@ int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const in
 void oracle_set_proj_mode(int mode);
 
 /* Plan of a query type: n nodes in children-before-parent order.
-   op[k] (0 anchor, 1 projection, 2 and, 3 or), child[3k..3k+2] (-1 unused),
+   op[k] (0 anchor, 1 projection, 2 and, 3 or, 4 complement), child[3k..3k+2] (-1 unused),
    slot[k] (anchor slot, relation slot, or -1).  Returns n. */
 int oracle_type_plan(int qtype, int32_t *op, int32_t *child, int32_t *slot, int32_t *root);
 

@@ -18,7 +18,7 @@ import pytest
 from oracle import brute
 import kgsynth
 
-TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
 
 
 def tiny_graph(seed, V=9, R=3, n=30, inverse=False):
@@ -99,8 +99,8 @@ def test_sample_invariants_against_brute_force(oracle_lib, qtype):
             assert out["positive"][b] in ans
             # anchors/relations used by the shape are set, unused are -1
             used = {"1p": 1, "2p": 1, "3p": 1, "2i": 2, "3i": 3, "ip": 2, "pi": 2, "2u": 2,
-                    "up": 2}[qtype]
-            nrel = {"1p": 1, "2p": 2, "3p": 3, "2i": 2, "2u": 2}.get(qtype, 3)
+                    "up": 2, "2in": 2, "3in": 3, "inp": 2, "pin": 2, "pni": 2}[qtype]
+            nrel = {"1p": 1, "2p": 2, "3p": 3, "2i": 2, "2u": 2, "2in": 2}.get(qtype, 3)
             assert (a[:used] >= 0).all() and (a[used:] == -1).all()
             assert (r[:nrel] >= 0).all() and (r[nrel:] == -1).all()
             # edges touching the anchors exist (witness of the grounding)

@@ -20,7 +20,7 @@ import pytest
 import kgsynth
 from oracle import cuts as C
 
-TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
 
 
 @pytest.mark.parametrize("qtype", TYPES)

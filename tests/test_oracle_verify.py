@@ -5,8 +5,9 @@ sampling, Sec. 3.2) and of its use for evaluation on nested graphs
 - Mask bits against brute-force answer sets of the first-order formulas
   (Sec. 2, Def. of logical queries) for random candidates, including ids
   outside [0, V), which are never negatives.
-- Monotonicity on nested graphs: adding edges can only add answers, so a
-  candidate that is a non-answer on the larger graph is one on the smaller.
+- Monotonicity on nested graphs for the shapes without negation: adding
+  edges can only add answers there, so a candidate that is a non-answer on
+  the larger graph is one on the smaller.
 - A query's own positive is an answer of the graph it was sampled on.
 """
 import numpy as np
@@ -15,7 +16,7 @@ import pytest
 import kgsynth
 from oracle import brute
 
-TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
 
 
 def bits(mask, n):
@@ -45,7 +46,9 @@ def test_verify_against_brute_force(oracle_lib, qtype):
         assert out["n_valid"][i] == sum(want)
 
 
-@pytest.mark.parametrize("qtype", TYPES)
+# Adding edges can also grow a negated operand's set, so a shape with
+# negation may lose answers on the larger graph: monotone only without it.
+@pytest.mark.parametrize("qtype", TYPES[:9])
 def test_verify_is_monotone_on_nested_graphs(oracle_lib, qtype):
     rng = np.random.default_rng(91)
     V, R = 300, 4
