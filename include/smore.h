@@ -31,7 +31,7 @@ enum {
     SMORE_OK = 0,
     SMORE_E_INVALID_ARG = -1, /* null pointer, bad size, bad query plan */
     SMORE_E_RANGE = -2,       /* an id outside [0, V) or [0, R) */
-    SMORE_E_UNSUPPORTED = -3, /* plan outside the nine shapes, negation, limits */
+    SMORE_E_UNSUPPORTED = -3, /* plan outside the fourteen shapes, limits */
     SMORE_E_NOMEM = -4,       /* device or host allocation failed */
     SMORE_E_HIP = -5,         /* a HIP runtime call failed */
     SMORE_E_OVERFLOW = -6     /* counts beyond the int32 / 32-bit query-id range */
@@ -43,7 +43,8 @@ enum {
 /* Node operators of a query computation plan (Sec. 2, "Query computation
    plan"; appendix on the computation plan).  Each node is a set of
    entities; a projection node applies one relation to its single child, an
-   intersection / union node combines its children, an anchor is a leaf. */
+   intersection / union node combines its children, a complement node is
+   V minus its single child, an anchor is a leaf. */
 enum { SMORE_OP_ANCHOR = 0, SMORE_OP_PROJ = 1, SMORE_OP_AND = 2, SMORE_OP_OR = 3, SMORE_OP_NOT = 4 };
 
 /* One plan node.  child[] index earlier nodes of the same plan (children
@@ -123,10 +124,12 @@ int smore_graph_info(const smore_graph *g, int64_t *n_entities, int64_t *n_relat
    Synchronous. */
 int smore_graph_copy(const smore_graph *g, int32_t which, int32_t *host_dst, int64_t count);
 
-/* Fill *out with one of the nine negation-free shapes "1p" "2p" "3p" "2i"
-   "3i" "ip" "pi" "2u" "up" (Sec. 5.1: the query structures of BetaE).
-   Anchor and relation slots follow branch order, and within a branch run
-   from the anchor to the root. */
+/* Fill *out with one of the fourteen query structures of BetaE (Sec. 5.1):
+   the nine without negation "1p" "2p" "3p" "2i" "3i" "ip" "pi" "2u" "up",
+   and "2in" "3in" "inp" "pin" "pni", where one operand of the intersection
+   is complemented (2in, 3in, inp, pin: the last one-hop operand; pni: the
+   two-hop operand).  Anchor and relation slots follow branch order, and
+   within a branch run from the anchor to the root. */
 int smore_query_preset(const char *name, smore_query_dag *out);
 
 /* Node cut of a plan tree minimising the worst per-anchor-path cost
@@ -159,9 +162,15 @@ int smore_sample_workspace_bytes(const smore_graph *g, const smore_query_dag *da
    than max_fanout wins.  Candidate j (j < neg_tries) is uniform over all V
    entities and is kept iff it is not an answer of the query and was not
    drawn earlier; the first n_neg kept are returned.  Draws come from
-   Philox4x32-10 with counter (j, t, q, tag) and key seed.  The plan must
-   be one of the nine presets (SMORE_E_UNSUPPORTED otherwise, including
-   negation).  hip_stream: a hipStream_t, or NULL for the default stream. */
+   Philox4x32-10 with counter (j, t, q, tag) and key seed.
+   A complemented operand of an intersection (the negation shapes) is
+   grounded after the positive operands, from a sibling entity w drawn
+   uniformly from A_r(x) of the first positive operand's step (x, r) -> e;
+   the attempt is also rejected when e lies in the complemented set, so the
+   root is always an answer.  Draws are numbered in grounding order (root,
+   two per projection, one for w).  The plan must be one of the fourteen
+   presets (SMORE_E_UNSUPPORTED otherwise).  hip_stream: a hipStream_t, or
+   NULL for the default stream. */
 int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_sample_args *args,
                  const smore_sample_out *out, void *workspace, size_t ws_bytes, void *hip_stream);
 

@@ -17,7 +17,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsmore.so")
 
-TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up")
+TYPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
 ADD_INVERSE = 1
 MAX_NEG_TRIES = 4096
 OP_ANCHOR, OP_PROJ, OP_AND, OP_OR, OP_NOT = range(5)

@@ -1,5 +1,5 @@
 // capi.cpp -- host side of the C ABI declared in include/smore.h: argument
-// validation, the nine plan presets, the node-cut planner, compilation of a
+// validation, the fourteen plan presets, the node-cut planner, compilation of a
 // plan into the positive-sampling program, and graph handle management.
 // Device work is in graph_build.hip and sample.hip.
 #include <hip/hip_runtime.h>
@@ -34,17 +34,20 @@ int ok()
 }
 
 // ----------------------------------------------------------- plan presets
-// The nine negation-free query structures (Sec. 5.1, the shapes of BetaE)
-// as computation-plan trees, children listed before parents.
+// The fourteen query structures of the experiments (Sec. 5.1, the shapes
+// of BetaE) as computation-plan trees, children listed before parents: nine
+// without negation, then five whose intersection has one complemented
+// operand (complement is a plan operator, appendix on the computation plan).
 smore_dag_node anchor(int slot) { return {SMORE_OP_ANCHOR, 0, {-1, -1, -1}, slot}; }
 smore_dag_node proj(int c, int slot) { return {SMORE_OP_PROJ, 1, {c, -1, -1}, slot}; }
 smore_dag_node both(int op, int a, int b) { return {op, 2, {a, b, -1}, -1}; }
+smore_dag_node neg(int c) { return {SMORE_OP_NOT, 1, {c, -1, -1}, -1}; }
 
 struct Preset {
     const char* name;
     smore::QType qt;
     int n;
-    smore_dag_node nd[7];
+    smore_dag_node nd[8];
 };
 
 const Preset kPresets[smore::NQTYPE] = {
@@ -62,12 +65,24 @@ const Preset kPresets[smore::NQTYPE] = {
     {"2u", smore::Q2U, 5, {anchor(0), proj(0, 0), anchor(1), proj(2, 1), both(SMORE_OP_OR, 1, 3)}},
     {"up", smore::QUP, 6,
      {anchor(0), proj(0, 0), anchor(1), proj(2, 1), both(SMORE_OP_OR, 1, 3), proj(4, 2)}},
+    {"2in", smore::Q2IN, 6,
+     {anchor(0), proj(0, 0), anchor(1), proj(2, 1), neg(3), both(SMORE_OP_AND, 1, 4)}},
+    {"3in", smore::Q3IN, 8,
+     {anchor(0), proj(0, 0), anchor(1), proj(2, 1), anchor(2), proj(4, 2), neg(5),
+      {SMORE_OP_AND, 3, {1, 3, 6}, -1}}},
+    {"inp", smore::QINP, 7,
+     {anchor(0), proj(0, 0), anchor(1), proj(2, 1), neg(3), both(SMORE_OP_AND, 1, 4), proj(5, 2)}},
+    {"pin", smore::QPIN, 7,
+     {anchor(0), proj(0, 0), proj(1, 1), anchor(1), proj(3, 2), neg(4), both(SMORE_OP_AND, 2, 5)}},
+    {"pni", smore::QPNI, 7,
+     {anchor(0), proj(0, 0), proj(1, 1), neg(2), anchor(1), proj(4, 2), both(SMORE_OP_AND, 3, 5)}},
 };
 
 // Node cut the verification kernel of each shape is written for: the cut the
 // planner returns with tie_break 0 on the preset (node indices).
 const int kKernelCut[smore::NQTYPE][4] = {
     {1, 0}, {1, 1}, {1, 1}, {2, 0, 2}, {3, 0, 2, 4}, {2, 1, 3}, {2, 1, 3}, {2, 0, 2}, {2, 1, 3},
+    {2, 0, 2}, {3, 0, 2, 4}, {2, 1, 3}, {2, 1, 3}, {2, 1, 4},
 };
 
 // Structural validation: a tree whose children precede their parent, with
@@ -199,7 +214,11 @@ struct Planner {
     }
 };
 
-// Pre-order walk program of reverse directional sampling (Sec. 3.1).
+// Walk program of reverse directional sampling (Sec. 3.1): pre-order, an
+// intersection's positive operands first; its complemented operand (the
+// presets have at most one, a chain of projections down to an anchor) is
+// grounded from the sibling entity drawn from the first positive operand's
+// step (the oracle's reading of how a negated operand is grounded).
 void compile_walk(const smore_query_dag* d, int v, int reg, smore::WalkProgram* w)
 {
     const smore_dag_node& nd = d->node[v];
@@ -215,7 +234,33 @@ void compile_walk(const smore_query_dag* d, int v, int reg, smore::WalkProgram* 
         compile_walk(d, nd.child[0], k + 1, w);
         return;
     }
-    for (int c = 0; c < nd.n_child; ++c) compile_walk(d, nd.child[c], reg, w);
+    if (nd.op == SMORE_OP_NOT) {
+        compile_walk(d, nd.child[0], reg, w);
+        return;
+    }
+    int first_pos = -1;
+    for (int c = 0; c < nd.n_child; ++c) {
+        if (d->node[nd.child[c]].op == SMORE_OP_NOT) continue;
+        if (first_pos < 0) first_pos = w->n_steps;
+        compile_walk(d, nd.child[c], reg, w);
+    }
+    for (int c = 0; c < nd.n_child; ++c) {
+        const int n = nd.child[c];
+        if (d->node[n].op != SMORE_OP_NOT) continue;
+        w->neg_first = w->n_steps;
+        w->sib_step = first_pos;
+        w->neg_target = reg;
+        compile_walk(d, n, smore::WALK_SIB, w);
+        w->neg_steps = w->n_steps - w->neg_first;
+        // the operand's chain: relations outermost first, then its anchor
+        int x = d->node[n].child[0], depth = 0, rels[2] = {-1, -1};
+        while (d->node[x].op == SMORE_OP_PROJ && depth < 2) {
+            rels[depth++] = d->node[x].slot;
+            x = d->node[x].child[0];
+        }
+        w->neg_anchor = d->node[x].slot;
+        for (int k = 0; k < depth; ++k) w->neg_rel[k] = rels[depth - 1 - k];
+    }
     for (int a = 0; a < nd.n_child; ++a)
         for (int b = a + 1; b < nd.n_child; ++b) {
             const smore_dag_node &x = d->node[nd.child[a]], &y = d->node[nd.child[b]];
@@ -247,7 +292,8 @@ int smore_query_preset(const char* name, smore_query_dag* out)
             for (int k = 0; k < p.n; ++k) out->node[k] = p.nd[k];
             return ok();
         }
-    return fail(SMORE_E_UNSUPPORTED, "unknown query shape '%s' (1p 2p 3p 2i 3i ip pi 2u up)", name);
+    return fail(SMORE_E_UNSUPPORTED,
+                "unknown query shape '%s' (1p 2p 3p 2i 3i ip pi 2u up 2in 3in inp pin pni)", name);
 }
 
 int smore_plan(const smore_query_dag* dag, int32_t tie_break, int32_t* cut_nodes, int32_t* n_cut)
@@ -393,14 +439,11 @@ int check_args(const smore_query_dag* dag, const smore_sample_args* a, int* qt_o
 {
     int rc = check_dag(dag);
     if (rc) return rc;
-    for (int k = 0; k < dag->n_nodes; ++k)
-        if (dag->node[k].op == SMORE_OP_NOT)
-            return fail(SMORE_E_UNSUPPORTED, "negation is not supported by the sampler");
     int qt = -1;
     for (const Preset& p : kPresets)
         if (same_dag(dag, p)) qt = p.qt;
     if (qt < 0)
-        return fail(SMORE_E_UNSUPPORTED, "plan is not one of the nine presets (use smore_query_preset)");
+        return fail(SMORE_E_UNSUPPORTED, "plan is not one of the fourteen presets (use smore_query_preset)");
     if (a->batch < 1) return fail(SMORE_E_INVALID_ARG, "batch must be >= 1");
     if (a->n_neg < 0) return fail(SMORE_E_INVALID_ARG, "n_neg must be >= 0");
     if (a->pos_tries < 1) return fail(SMORE_E_INVALID_ARG, "pos_tries must be >= 1");

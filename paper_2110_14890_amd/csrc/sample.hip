@@ -311,10 +311,76 @@ __device__ bool wave_meet3(const int32_t* S, int32_t ns, FSet A, FSet B, int lan
     return false;
 }
 
+// Does the sorted graph list S share an element with A that is not in B
+// (the set difference of an intersection with a complemented operand)?
+// The shorter of S and A is the key list, searched in the other and in B.
+template <class T>
+__device__ bool wave_meet_minus(const int32_t* S, int32_t ns, FSet A, FSet B, int lane, T& tl)
+{
+    const int32_t *K = S, *L = A.p;
+    int32_t nk = ns, nl = A.n;
+    bool kg = true, lg = false;   // lookups inside forward lists are not counted
+    if (A.n < ns) {
+        K = A.p; nk = A.n; kg = false;
+        L = S; nl = ns; lg = true;
+    }
+    for (int32_t k0 = 0; k0 < nk; k0 += 256) {
+        int32_t x[4];
+        bool f1[4], f2[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int32_t i = k0 + 64 * k + lane;
+            x[k] = i < nk ? K[i] : -1;
+        }
+        if (kg && lane == 0) tl.read(K + k0, 4 * min(256, nk - k0));
+        search4(L, nl, x, f1, lg, tl);
+        search4(B.p, B.n, x, f2, false, tl);
+        const bool hit = (f1[0] && !f2[0]) || (f1[1] && !f2[1]) || (f1[2] && !f2[2]) || (f1[3] && !f2[3]);
+        if (__ballot(hit)) return true;
+    }
+    return false;
+}
+
 // ------------------------------------------------------------- positive
 __device__ __forceinline__ int32_t sel4(int i, int32_t a, int32_t b, int32_t c, int32_t d)
 {
     return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
+}
+
+__device__ __forceinline__ int32_t reg5(int i, const int32_t* e)
+{
+    return i == 0 ? e[0] : i == 1 ? e[1] : i == 2 ? e[2] : i == 3 ? e[3] : e[4];
+}
+
+// Relation grounded for relation slot sl (-1 if no step has it).
+__device__ __forceinline__ int32_t slot_rel(const WalkProgram& wp, const int32_t* qr, int sl)
+{
+    int32_t v = -1;
+    for (int k = 0; k < wp.n_steps; ++k)
+        if (wp.rel_slot[k] == sl) v = sel4(k, qr[0], qr[1], qr[2], -1);
+    return v;
+}
+
+// Is t in the complemented operand's set: A_r0(a) for one step, or the
+// entities reached from A_r0(a) under r1 for two (some y of A_r0(a) with
+// (y, r1, t) an edge)?  At lane level: the shorter of A_r0(a) and t's
+// in-list under r1 is walked and each entry searched in the longer.
+__device__ bool neg_member(const GraphView& g, int steps, int32_t a, int32_t r0, int32_t r1, int32_t t)
+{
+    NoTally none;
+    const int2 f = group_range(g.fwd, a, r0);
+    const int32_t nf = f.y - f.x;
+    if (steps == 1) return nf > 0 && has(g.fwd.nbr + f.x, nf, t, false, none);
+    const int2 b = group_range(g.rev, t, r1);
+    const int32_t nb = b.y - b.x;
+    if (nf == 0 || nb == 0) return false;
+    const bool fk = nf <= nb;
+    const int32_t* K = fk ? g.fwd.nbr + f.x : g.rev.nbr + b.x;
+    const int32_t* L = fk ? g.rev.nbr + b.x : g.fwd.nbr + f.x;
+    const int32_t nk = fk ? nf : nb, nl = fk ? nb : nf;
+    for (int32_t i = 0; i < nk; ++i)
+        if (has(L, nl, K[i], false, none)) return true;
+    return false;
 }
 
 // Attempts of one query run PA at a time, on PA neighbouring lanes (lane l
@@ -328,16 +394,28 @@ __device__ __forceinline__ bool pos_attempt(const GraphView& g, const WalkProgra
                                             const SampleParams& p, uint32_t q, int t, int32_t* e,
                                             int32_t* qr)
 {
-    e[0] = e[1] = e[2] = e[3] = -1;
+    e[0] = e[1] = e[2] = e[3] = e[4] = -1;
     qr[0] = qr[1] = qr[2] = -1;
     if (g.n_active == 0) return false;
     e[0] = g.active_in[reduce_range(draw64(p.seed, TAG_POS, q, t, 0), (uint32_t)g.n_active)];
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
         if (k >= wp.n_steps) break;
-        const int32_t v = sel4(wp.src[k], e[0], e[1], e[2], e[3]);
-        const uint64_t u0 = draw64(p.seed, TAG_POS, q, t, 1 + 2 * k);
-        const uint64_t u1 = draw64(p.seed, TAG_POS, q, t, 2 + 2 * k);
+        const bool sib = wp.neg_steps > 0 && k == wp.neg_first;
+        const int after = wp.neg_steps > 0 && k >= wp.neg_first ? 1 : 0;
+        if (sib) {
+            // sibling entity of the complemented operand: uniform over
+            // A_r(x) of step sib_step, a list that holds that step's entity
+            const int32_t x = reg5(wp.sib_step + 1, e);
+            const int32_t r = sel4(wp.sib_step, qr[0], qr[1], qr[2], -1);
+            const int2 fr = group_range(g.fwd, x, r);
+            if (fr.y == fr.x) return false;
+            const uint64_t u = draw64(p.seed, TAG_POS, q, t, 1 + 2 * k);
+            e[WALK_SIB] = g.fwd.nbr[fr.x + (int32_t)reduce_range(u, (uint32_t)(fr.y - fr.x))];
+        }
+        const int32_t v = reg5(wp.src[k], e);
+        const uint64_t u0 = draw64(p.seed, TAG_POS, q, t, 1 + 2 * k + after);
+        const uint64_t u1 = draw64(p.seed, TAG_POS, q, t, 2 + 2 * k + after);
         const int32_t s0 = g.rev.node[v], s1 = g.rev.node[v + 1];
         if (s0 == s1) return false;                       // no in-edge: dead end
         const int32_t s = s0 + (int32_t)reduce_range(u0, (uint32_t)(s1 - s0));
@@ -352,15 +430,17 @@ __device__ __forceinline__ bool pos_attempt(const GraphView& g, const WalkProgra
         qr[k] = gr.x;
     }
     for (int pr = 0; pr < wp.n_pairs; ++pr) {
-        const int32_t xa = sel4(wp.anchor_reg[wp.pair_anchor[pr][0]], e[0], e[1], e[2], e[3]);
-        const int32_t xb = sel4(wp.anchor_reg[wp.pair_anchor[pr][1]], e[0], e[1], e[2], e[3]);
-        int32_t ra = -1, rb = -1;
-        for (int k = 0; k < wp.n_steps; ++k) {
-            const int32_t rk = sel4(k, qr[0], qr[1], qr[2], -1);
-            if (wp.rel_slot[k] == wp.pair_rel[pr][0]) ra = rk;
-            if (wp.rel_slot[k] == wp.pair_rel[pr][1]) rb = rk;
-        }
+        const int32_t xa = reg5(wp.anchor_reg[wp.pair_anchor[pr][0]], e);
+        const int32_t xb = reg5(wp.anchor_reg[wp.pair_anchor[pr][1]], e);
+        const int32_t ra = slot_rel(wp, qr, wp.pair_rel[pr][0]);
+        const int32_t rb = slot_rel(wp, qr, wp.pair_rel[pr][1]);
         if (xa == xb && ra == rb) return false;           // degenerate sibling branches
+    }
+    if (wp.neg_steps > 0) {   // the intersection's entity must stay outside the complemented set
+        const int32_t a = reg5(wp.anchor_reg[wp.neg_anchor], e);
+        const int32_t r0 = slot_rel(wp, qr, wp.neg_rel[0]);
+        const int32_t r1 = wp.neg_steps > 1 ? slot_rel(wp, qr, wp.neg_rel[1]) : -1;
+        if (neg_member(g, wp.neg_steps, a, r0, r1, reg5(wp.neg_target, e))) return false;
     }
     return true;
 }
@@ -374,7 +454,7 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
     if (b >= p.batch) return;   // whole groups: PA divides the workgroup size
     const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
     const int gbase = (threadIdx.x & 63) & ~(PA - 1);
-    int32_t e[4], qr[3];
+    int32_t e[5], qr[3];
     int win = -1;
     for (int t0 = 0; t0 < p.pos_tries; t0 += PA) {
         const int t = t0 + l;
@@ -399,13 +479,8 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
     if (l != win % PA) return;  // the lane that ran the winning attempt writes the row
     int32_t* A = out.anchors + 3 * (int64_t)b;
     int32_t* R = out.relations + 3 * (int64_t)b;
-    for (int a = 0; a < 3; ++a) A[a] = a < wp.n_anchor ? sel4(wp.anchor_reg[a], e[0], e[1], e[2], e[3]) : -1;
-    for (int sl = 0; sl < 3; ++sl) {
-        int32_t v = -1;
-        for (int k = 0; k < wp.n_steps; ++k)
-            if (wp.rel_slot[k] == sl) v = sel4(k, qr[0], qr[1], qr[2], -1);
-        R[sl] = v;
-    }
+    for (int a = 0; a < 3; ++a) A[a] = a < wp.n_anchor ? reg5(wp.anchor_reg[a], e) : -1;
+    for (int sl = 0; sl < 3; ++sl) R[sl] = slot_rel(wp, qr, sl);
     out.positive[b] = e[0];
     out.n_valid[b] = 0;
     out.pos_attempts[b] = win + 1;
@@ -426,7 +501,8 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
 // device-side list, so rounds need no host synchronisation.
 
 // Lists per shape (anchor slot, relation slot) at the cut the planner picks:
-//   1p {a0}, 2p/3p {V1}, 2i/3i/2u {anchors}, ip/up {Y0, Y1}, pi {V1, a1}.
+//   1p {a0}, 2p/3p {V1}, 2i/3i/2u/2in/3in {anchors}, ip/up/inp {Y0, Y1},
+//   pi/pin {V1, a1}, pni {V1 of the complemented chain, a1}.
 // cached = forward caching to the cut (A_r(a) at a cut node one projection
 // above the anchor); otherwise the list is the anchor's neighbour list used
 // for an edge test at a cut placed on the anchor, which may be decided from
@@ -446,7 +522,18 @@ SHAPE(QIP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
 SHAPE(QPI, 2, 2, 3, 0, 1, 0, 0, 2, 0, 1, 0, 0)
 SHAPE(Q2U, 2, 2, 2, 0, 1, 0, 0, 1, 0, 0, 0, 0)
 SHAPE(QUP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
+SHAPE(Q2IN, 2, 2, 2, 0, 1, 0, 0, 1, 0, 0, 0, 0)
+SHAPE(Q3IN, 3, 3, 3, 0, 1, 2, 0, 1, 2, 0, 0, 0)
+SHAPE(QINP, 2, 2, 3, 0, 1, 0, 0, 1, 0, 1, 1, 0)
+SHAPE(QPIN, 2, 2, 3, 0, 1, 0, 0, 2, 0, 1, 0, 0)
+SHAPE(QPNI, 2, 2, 3, 0, 1, 0, 0, 2, 0, 1, 0, 0)
 #undef SHAPE
+
+// Shapes whose last step into the root is the backward step of a two-hop
+// chain under relation slot 1 (else slot 2), and shapes whose second list
+// is a forward-cached set the deep test needs staged.
+template <int QT> constexpr bool chain_r1 = QT == Q2P || QT == QPI || QT == QPIN || QT == QPNI;
+template <int QT> constexpr bool two_cached = QT == QIP || QT == QUP || QT == QINP;
 
 // Lists that test a candidate by one edge into the root: c is an answer
 // only if c is in list f for every f of `mask` (any f when `any`).  When
@@ -458,6 +545,10 @@ template <> struct RootLists<Q2I> { static constexpr int mask = 3, any = 0; };
 template <> struct RootLists<Q3I> { static constexpr int mask = 7, any = 0; };
 template <> struct RootLists<QPI> { static constexpr int mask = 2, any = 0; };
 template <> struct RootLists<Q2U> { static constexpr int mask = 3, any = 1; };
+// with negation, only the positive operands' lists are necessary conditions
+template <> struct RootLists<Q2IN> { static constexpr int mask = 1, any = 0; };
+template <> struct RootLists<Q3IN> { static constexpr int mask = 3, any = 0; };
+template <> struct RootLists<QPNI> { static constexpr int mask = 2, any = 0; };
 
 constexpr int CWG = 256;         // threads of the candidate and compaction workgroups
 constexpr int HEAVY_WG = 256;    // threads of the heavy-queue workgroups
@@ -577,12 +668,21 @@ __device__ __forceinline__ int32_t shallow_test(const GraphView& g, const FSet* 
     if (QT == Q2U)
         return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) ||
                 edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl)) ? ST_ANS : ST_NON;
-    if (QT == QPI && !edge_test(g, F[1], anc[1], rel[2], c, n0, n1, tl)) return ST_NON;
-    // backward step from c under the relation entering the root
-    const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
+    if (QT == Q2IN)
+        return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) &&
+                !edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl)) ? ST_ANS : ST_NON;
+    if (QT == Q3IN)
+        return (edge_test(g, F[0], anc[0], rel[0], c, n0, n1, tl) &&
+                edge_test(g, F[1], anc[1], rel[1], c, n0, n1, tl) &&
+                !edge_test(g, F[2], anc[2], rel[2], c, n0, n1, tl)) ? ST_ANS : ST_NON;
+    if ((QT == QPI || QT == QPNI) && !edge_test(g, F[1], anc[1], rel[2], c, n0, n1, tl)) return ST_NON;
+    if (QT == QPIN && edge_test(g, F[1], anc[1], rel[2], c, n0, n1, tl)) return ST_NON;
+    // backward step from c under the relation entering the root; for pni a
+    // meeting chain puts c in the complemented set
+    const int32_t rb = chain_r1<QT> ? rel[1] : rel[2];
     const int2 s = group_find(g.rev, n0, n1, rb, tl);
-    if (s.y == s.x) return ST_NON;
-    if (s.y - s.x > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) return ST_PEND;
+    if (s.y == s.x) return QT == QPNI ? ST_ANS : ST_NON;
+    if (s.y - s.x > LANE_SEG || !F[0].lds || (two_cached<QT> && !F[1].lds)) return ST_PEND;
     lst = s;
     return ST_DEEP;
 }
@@ -604,7 +704,7 @@ __device__ __forceinline__ void shallow_test2(const GraphView& g, const FSet* F,
             tl.read(g.rev.node + c[u], 8);
         }
     }
-    if (QT == Q1P || QT == Q2I || QT == Q3I || QT == Q2U) {
+    if (QT == Q1P || QT == Q2I || QT == Q3I || QT == Q2U || QT == Q2IN || QT == Q3IN) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
             st[u] = act[u] ? shallow_test<QT>(g, F, anc, rel, c[u], n0[u], n1[u], lst[u], tl) : ST_NON;
@@ -612,16 +712,25 @@ __device__ __forceinline__ void shallow_test2(const GraphView& g, const FSet* F,
     }
     bool live[2];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
-        live[u] = act[u] && (QT != QPI || edge_test(g, F[1], anc[1], rel[2], c[u], n0[u], n1[u], tl));
-    const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
+    for (int u = 0; u < 2; ++u) {
+        live[u] = act[u];
+        if (QT == QPI || QT == QPNI || QT == QPIN) {
+            const bool e = act[u] && edge_test(g, F[1], anc[1], rel[2], c[u], n0[u], n1[u], tl);
+            live[u] = act[u] && (QT == QPIN ? !e : e);
+        }
+    }
+    const int32_t rb = chain_r1<QT> ? rel[1] : rel[2];
     int2 sr[2];
     group_find2(g.rev, n0, n1, live, rb, sr, tl);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
         st[u] = ST_NON;
-        if (!live[u] || sr[u].y == sr[u].x) continue;
-        if (sr[u].y - sr[u].x > LANE_SEG || !F[0].lds || ((QT == QIP || QT == QUP) && !F[1].lds)) {
+        if (!live[u]) continue;
+        if (sr[u].y == sr[u].x) {
+            if (QT == QPNI) st[u] = ST_ANS;   // nothing reaches c through the complemented chain
+            continue;
+        }
+        if (sr[u].y - sr[u].x > LANE_SEG || !F[0].lds || (two_cached<QT> && !F[1].lds)) {
             st[u] = ST_PEND;
         } else {
             lst[u] = sr[u];
@@ -646,11 +755,13 @@ __device__ __forceinline__ int32_t deep_test(const GraphView& g, const FSet* F, 
 #pragma unroll
         for (int k = 0; k < LANE_SEG; ++k) {
             if (k >= len) break;
-            if (QT == Q2P || QT == QPI) hit = hit || has(F[0], y[k], tl);
+            if (chain_r1<QT>) hit = hit || has(F[0], y[k], tl);
             else if (QT == QIP) hit = hit || (has(F[0], y[k], tl) && has(F[1], y[k], tl));
+            else if (QT == QINP) hit = hit || (has(F[0], y[k], tl) && !has(F[1], y[k], tl));
             else hit = hit || has(F[0], y[k], tl) || has(F[1], y[k], tl);
         }
-        return hit ? ST_ANS : ST_NON;
+        // pni: a meeting chain means c is in the complemented set
+        return (QT == QPNI ? !hit : hit) ? ST_ANS : ST_NON;
     }
     // 3p: node pairs of every y at once, then each y's group under r1
     int32_t a0[LANE_SEG], a1[LANE_SEG];
@@ -681,20 +792,22 @@ __device__ __forceinline__ int32_t deep_test(const GraphView& g, const FSet* F, 
     return ST_NON;
 }
 
-// Wavefront decision for a queued candidate (the one-hop branch of pi has
-// already passed at lane level).
+// Wavefront decision for a queued candidate (the one-hop operand of
+// pi / pin / pni has already been tested at lane level).
 template <int QT, class T>
 __device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel, int32_t c, int lane,
                            T& tl)
 {
-    const int32_t rb = (QT == Q2P || QT == QPI) ? rel[1] : rel[2];
+    const int32_t rb = chain_r1<QT> ? rel[1] : rel[2];
     int2 s = group_range(g.rev, c, rb, tl);   // same address in every lane
     s.x = uni(s.x);
     s.y = uni(s.y);
     const int32_t* S = g.rev.nbr + s.x;
     const int32_t ns = s.y - s.x;
-    if (QT == Q2P || QT == QPI) return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl);
+    if (QT == Q2P || QT == QPI || QT == QPIN) return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl);
+    if (QT == QPNI) return !wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl);
     if (QT == QIP) return wave_meet3(S, ns, F[0], F[1], lane, tl);
+    if (QT == QINP) return wave_meet_minus(S, ns, F[0], F[1], lane, tl);
     if (QT == QUP)
         return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl) ||
                wave_meet(S, ns, true, F[1].p, F[1].n, false, lane, tl);
@@ -1339,6 +1452,11 @@ int dispatch_negatives(QType qt, const GraphView& gv, const SampleParams& p, con
         case QPI: return run_negatives<QPI, T>(gv, p, out, ws, stats, R, st, err);
         case Q2U: return run_negatives<Q2U, T>(gv, p, out, ws, stats, R, st, err);
         case QUP: return run_negatives<QUP, T>(gv, p, out, ws, stats, R, st, err);
+        case Q2IN: return run_negatives<Q2IN, T>(gv, p, out, ws, stats, R, st, err);
+        case Q3IN: return run_negatives<Q3IN, T>(gv, p, out, ws, stats, R, st, err);
+        case QINP: return run_negatives<QINP, T>(gv, p, out, ws, stats, R, st, err);
+        case QPIN: return run_negatives<QPIN, T>(gv, p, out, ws, stats, R, st, err);
+        case QPNI: return run_negatives<QPNI, T>(gv, p, out, ws, stats, R, st, err);
         default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
     }
 }
@@ -1472,6 +1590,11 @@ int dispatch_pairs(QType qt, const GraphView& gv, const SampleParams& p, const s
         case QPI: return run_pairs<QPI>(gv, p, q, ws, mask, R, st, err);
         case Q2U: return run_pairs<Q2U>(gv, p, q, ws, mask, R, st, err);
         case QUP: return run_pairs<QUP>(gv, p, q, ws, mask, R, st, err);
+        case Q2IN: return run_pairs<Q2IN>(gv, p, q, ws, mask, R, st, err);
+        case Q3IN: return run_pairs<Q3IN>(gv, p, q, ws, mask, R, st, err);
+        case QINP: return run_pairs<QINP>(gv, p, q, ws, mask, R, st, err);
+        case QPIN: return run_pairs<QPIN>(gv, p, q, ws, mask, R, st, err);
+        case QPNI: return run_pairs<QPNI>(gv, p, q, ws, mask, R, st, err);
         default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
     }
 }

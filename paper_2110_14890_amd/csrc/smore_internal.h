@@ -28,12 +28,23 @@ struct GraphView {
     int32_t n_active;
 };
 
-// Positive-sampling program compiled from a plan on the host: a pre-order
-// list of projection steps.  Register 0 holds the root; step k reads
-// register src[k], grounds relation slot rel_slot[k] and writes register
-// k + 1.  Anchor slot a takes register anchor_reg[a].  Pairs of single-
-// projection siblings under an intersection or union must differ in
-// (anchor, relation).
+// Positive-sampling program compiled from a plan on the host: the
+// projection steps in grounding order (pre-order, an intersection's
+// positive operands before its complemented one).  Register 0 holds the
+// root; step k reads register src[k], grounds relation slot rel_slot[k]
+// and writes register k + 1.  Anchor slot a takes register anchor_reg[a].
+// Pairs of single-projection siblings under an intersection or union must
+// differ in (anchor, relation).
+//
+// A complemented operand (neg_steps > 0): before step neg_first, register
+// WALK_SIB takes the sibling entity w, one draw uniform over A_r(x) of
+// step sib_step ((x, r) = its register sib_step + 1 and its relation);
+// steps neg_first .. neg_first + neg_steps - 1 ground the operand from w;
+// after the walk, register neg_target must lie outside the operand's set,
+// the chain from anchor slot neg_anchor through relation slots neg_rel[0]
+// (innermost) .. neg_rel[neg_steps - 1].  Draws are numbered in grounding
+// order: 0 for the root, two per step, one for w.
+constexpr int WALK_SIB = 4;
 struct WalkProgram {
     int32_t n_steps;
     int32_t src[3];
@@ -43,10 +54,13 @@ struct WalkProgram {
     int32_t n_pairs;
     int32_t pair_anchor[3][2];
     int32_t pair_rel[3][2];
+    int32_t neg_steps, neg_first, sib_step, neg_target, neg_anchor;
+    int32_t neg_rel[2];
 };
 
-// Query shapes with a dedicated verification kernel.
-enum QType { Q1P = 0, Q2P, Q3P, Q2I, Q3I, QIP, QPI, Q2U, QUP, NQTYPE };
+// Query shapes with a dedicated verification kernel: the nine without
+// negation, then 2in 3in inp pin pni.
+enum QType { Q1P = 0, Q2P, Q3P, Q2I, Q3I, QIP, QPI, Q2U, QUP, Q2IN, Q3IN, QINP, QPIN, QPNI, NQTYPE };
 
 struct SampleParams {
     int32_t batch, n_neg, pos_tries, neg_tries, max_fanout;

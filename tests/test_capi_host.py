@@ -1,7 +1,7 @@
 """Host-side tests of the C ABI (no GPU needed).
 
 - the library loads and exports every function include/smore.h declares;
-- the nine presets encode the same plans as the oracle's (Sec. 2 plans);
+- the fourteen presets encode the same plans as the oracle's (Sec. 2 plans);
 - the planner (appendix on the optimal cut: DP over u, s, o plus top-down
   construction) returns a node cut (Def. "Node cut") whose cost equals the
   brute-force minimum of the optimal-scheduling objective, for the presets
@@ -61,10 +61,13 @@ def test_presets_match_oracle_plans(L, oracle_lib, qtype):
     assert op == list(oop) and ch == och.tolist() and sl == list(osl) and root == oroot
 
 
+# cuts worked out by hand from the DP (complement edges add no projection)
 STRICT_CUTS = {"1p": [0], "2p": [1], "3p": [1], "2i": [0, 2], "3i": [0, 2, 4], "ip": [1, 3],
-               "pi": [1, 3], "2u": [0, 2], "up": [1, 3]}
+               "pi": [1, 3], "2u": [0, 2], "up": [1, 3],
+               "2in": [0, 2], "3in": [0, 2, 4], "inp": [1, 3], "pin": [1, 3], "pni": [1, 4]}
 FORWARD_CUTS = {"1p": [1], "2p": [1], "3p": [2], "2i": [4], "3i": [6], "ip": [4], "pi": [1, 4],
-                "2u": [4], "up": [4]}
+                "2u": [4], "up": [4],
+                "2in": [5], "3in": [7], "inp": [5], "pin": [1, 5], "pni": [1, 5]}
 
 
 @pytest.mark.parametrize("qtype", TYPES)

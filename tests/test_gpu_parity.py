@@ -111,7 +111,7 @@ def test_budget_exhaustion_and_small_graphs(qt):
         assert_same(got, ref, what=f"{qt} n_neg {n_neg} neg_tries {nt} pos_tries {pt}")
 
 
-@pytest.mark.parametrize("qt", ["1p", "2p", "3p", "ip", "pi", "up"])
+@pytest.mark.parametrize("qt", ["1p", "2p", "3p", "ip", "pi", "up", "inp", "pin", "pni"])
 def test_max_fanout(qt):
     cfg, tr = config_graph("fb15k237")
     g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations)
@@ -125,7 +125,7 @@ def test_graph_without_in_edges_of_depth():
     # no entity can be reached twice: every 2p/3p walk dies, 1p succeeds
     tr = np.array([[0, 0, 1], [2, 0, 3], [4, 1, 5]], np.int32)
     g, og = graph_pair(tr, 6, 2)
-    for qt in ("1p", "2p", "3p", "2i", "ip"):
+    for qt in ("1p", "2p", "3p", "2i", "ip", "2in", "pni"):
         got = gpu_sample(g, qt, 9, 2, pos_tries=5, neg_tries=6)
         ref = og.sample(qt, 9, 2, pos_tries=5, neg_tries=6)
         assert_same(got, ref, what=qt)
@@ -157,13 +157,30 @@ def test_split_batch_and_repeat_are_identical():
             assert np.array_equal(full[k], out[k].cpu().numpy())
 
 
-def test_negation_plan_is_refused_on_device_graph():
+def test_plan_outside_the_presets_is_refused_on_device_graph():
+    # a complement at the root (not one of the fourteen structures)
     g = sm.Graph(np.array([[0, 0, 1]], np.int32), 2, 1)
     d = sm.query_preset("2p")
     d.node[2].op = sm.OP_NOT
     with pytest.raises(sm.SmoreError) as e:
         sm.sample(g, d, 2, 1)
     assert e.value.code == -3
+
+
+NEG_TYPES = ("2in", "3in", "inp", "pin", "pni")
+
+
+@pytest.mark.parametrize("name", ["fb15k237", "fb400k"])
+def test_negation_parity_full_batch(name):
+    # the five negation shapes on the skewed graphs, full batch
+    cfg, tr = config_graph(name)
+    g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
+    for qt in NEG_TYPES:
+        progress(f"{name} {qt} batch {cfg.batch} n_neg {cfg.n_neg}")
+        got = gpu_sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        ref = og.sample(qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        assert_same(got, ref, what=f"{name}/{qt}")
+        assert (got["n_valid"] >= 0).mean() > 0.5
 
 
 @pytest.mark.parametrize("name", ["wikikg2"])
@@ -173,7 +190,7 @@ def test_sample_parity_large_sampled_rows(name):
     cfg, tr = config_graph(name)
     g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
     rng = np.random.default_rng(0)
-    for qt in cfg.query_types:
+    for qt in cfg.query_types + NEG_TYPES:
         progress(f"{name} {qt}")
         got = gpu_sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
         rows = np.sort(rng.choice(cfg.batch, 96, replace=False))
