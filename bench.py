@@ -33,10 +33,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def workload_name(cfg):
+def workload_name(cfg, types):
     return (f"{cfg.name}-shaped synthetic KG: {cfg.n_entities:,} entities, "
             f"{cfg.n_relations:,} relations, {cfg.n_triples:,} triples; "
-            f"{'/'.join(cfg.query_types)} batch {cfg.batch:,}, {cfg.n_neg} negatives")
+            f"{'/'.join(types)} batch {cfg.batch:,}, {cfg.n_neg} negatives")
 
 
 def traffic_for(kernel):
@@ -100,7 +100,7 @@ def gather_ceiling(stream):
 def c_sweep(cfg, triples, g, threads, stream, seconds):
     """Time to sample one minibatch of 1,024 queries as a function of the
     maximum expansion C per relation (Sec. 5.2, sampler speed; the paper's
-    plots vary C on Freebase for 2p and ip): the GPU bidirectional sampler
+    plots vary C on Freebase for 2p, ip and pni): the GPU bidirectional sampler
     against the exhaustive CPU oracle on the same minibatches.  C bounds the
     width of every grounded step of the positive (max_fanout, rejection).
     The oracle runs until `seconds` per point, then its rate is
@@ -116,7 +116,7 @@ def c_sweep(cfg, triples, g, threads, stream, seconds):
     og = oracle.Graph(triples, cfg.n_entities, cfg.n_relations, cfg.add_inverse, threads=threads)
     log(f"oracle graph built in {time.time() - t0:.1f} s")
     mb, reps = 1024, 10
-    for qt in ("2p", "ip"):
+    for qt in ("2p", "ip", "pni"):
         dag = sm.query_preset(qt)
         for C in (10, 30, 100, 300, 1000, 3000, 0):
             args = [sm.make_args(mb, cfg.n_neg, seed=cfg.seed, query_offset=k * mb, max_fanout=C)
@@ -238,7 +238,7 @@ def main():
                     help="instead of the benchmark: minibatches sharing one candidate set")
     ap.add_argument("--c-sweep", action="store_true",
                     help="instead of the benchmark: minibatch time vs max expansion C, "
-                         "GPU vs the exhaustive CPU oracle (2p, ip)")
+                         "GPU vs the exhaustive CPU oracle (2p, ip, pni)")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -396,7 +396,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": workload_name(cfg), "types": types, "batch": cfg.batch,
+        "config": {"workload": workload_name(cfg, types), "types": types, "batch": cfg.batch,
                    "n_neg": cfg.n_neg, "neg_tries": neg_tries, "pos_tries": 64,
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed},
         "roofline": roofline,

@@ -3,8 +3,9 @@ triples), in the launch configuration bench.py times: the whole batch of
 16,384 queries x 512 negatives runs on the GPU; the oracle recomputes a
 random sample of rows one query at a time (its exhaustive answer sets make
 every query cost up to seconds here).  Also checks that the read-accounting
-variant of the verification kernel returns the same rows, and minibatches
-of 1,024 queries with a maximum expansion per relation."""
+variant of the verification kernel returns the same rows, the shapes with
+negation, and minibatches of 1,024 queries with a maximum expansion per
+relation."""
 import numpy as np
 import pytest
 
@@ -65,15 +66,32 @@ def test_freebase_sampled_rows_and_accounting(freebase):
 
 
 @pytest.mark.timeout(900)
+def test_freebase_negation_sampled_rows(freebase):
+    """The five shapes with negation on the whole batch (16,384 x 512),
+    sampled rows against the oracle."""
+    import paper_2110_14890_amd as sm
+
+    cfg, g, og = freebase
+    rng = np.random.default_rng(3)
+    for qt in ("2in", "3in", "inp", "pin", "pni"):
+        got = to_numpy(sm.sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed))
+        rows = np.sort(rng.choice(cfg.batch, 16, replace=False))
+        progress(f"{qt}: oracle on {len(rows)} sampled rows")
+        ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
+        assert_same(got, ref, rows=rows, what=f"freebase/{qt}")
+        progress(f"{qt}: ok, {int((got['n_valid'] == cfg.n_neg).sum())} complete queries")
+
+
+@pytest.mark.timeout(900)
 def test_freebase_max_expansion_minibatches(freebase):
     """Minibatches of 1,024 queries with a maximum expansion C per relation
     (max_fanout; the sampler-speed experiment of Sec. 5.2 varies C on
-    Freebase for 2p and ip): sampled rows against the oracle."""
+    Freebase for 2p, ip and pni): sampled rows against the oracle."""
     import paper_2110_14890_amd as sm
 
     cfg, g, og = freebase
     rng = np.random.default_rng(2)
-    for qt in ("2p", "ip"):
+    for qt in ("2p", "ip", "pni"):
         for C in (10, 300):
             got = to_numpy(sm.sample(g, qt, 1024, cfg.n_neg, seed=cfg.seed, query_offset=4096,
                                      max_fanout=C))
