@@ -892,56 +892,80 @@ __device__ __forceinline__ bool query_ok(const GraphView& g, const smore_sample_
 }
 
 // Per query: validity, forward-cached lists, staging plan, active list.
+// Four neighbouring lanes per query: lane f looks up list f, so the
+// dependent lookups of a query's lists run side by side; the staging plan
+// is made from the sizes of all its lists, in list order.
 template <int QT, class T>
 __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, smore_sample_out out,
                                                  Ws ws, int64_t* stats, int32_t R)
 {
-    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= p.batch) return;
-    if (b == 0) {   // queue and list counters of the first round: every query is listed
+    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t b = gid >> 2;
+    const int f = gid & 3;
+    if (b >= p.batch) return;   // whole groups: 4 divides the workgroup size
+    if (gid == 0) {   // queue and list counters of the first round: every query is listed
         ws.ctrl[0] = 0;
         ws.ctrl[1] = 0;
         ws.ctrl[2] = p.batch;
         ws.ctrl[3] = 0;
     }
-    ws.act[0][b] = b;
     int32_t anc[3], rel[3];
     int32_t* row = out.negatives + (int64_t)b * p.n_neg;
     int32_t* q = ws.qf + (int64_t)b * QF;
-    if (stats)
-        for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
+    if (f == 0) {
+        ws.act[0][b] = b;
+        if (stats)
+            for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
+    }
     if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
-        if (!p.shared_mode) {   // a shared-candidate minibatch has no per-query rows
-            for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
-            out.neg_draws[b] = -1;
+        if (f == 0) {
+            if (!p.shared_mode) {   // a shared-candidate minibatch has no per-query rows
+                for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
+                out.neg_draws[b] = -1;
+            }
+            out.n_valid[b] = -1;
+            q[6] = -1;   // skipped by the rounds
         }
-        out.n_valid[b] = -1;
-        q[6] = -1;   // skipped by the rounds
         return;
     }
     if (p.n_neg == 0) {
-        out.n_valid[b] = 0;
-        if (!p.shared_mode) out.neg_draws[b] = 0;
+        if (f == 0) {
+            out.n_valid[b] = 0;
+            if (!p.shared_mode) out.neg_draws[b] = 0;
+        }
         return;
     }
     T tl;
-    int32_t used = 0, staged = 0;
-    for (int f = 0; f < Shape<QT>::nf; ++f) {
-        const int2 r = group_range(g.fwd, anc[Shape<QT>::fa[f]], rel[Shape<QT>::fr[f]], tl);
+    int2 r = make_int2(0, 0);
+    if (f < Shape<QT>::nf) {
+        r = group_range(g.fwd, anc[Shape<QT>::fa[f]], rel[Shape<QT>::fr[f]], tl);
         q[2 * f] = r.x;
         q[2 * f + 1] = r.y;
-        const int32_t n = r.y - r.x;
-        if (n <= STAGE - used) {
-            staged |= 1 << f;
+    }
+    const int base = (threadIdx.x & 63) & ~3;
+    int32_t used = 0, staged = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        const int32_t n = __shfl(r.y - r.x, base + k);
+        if (k < Shape<QT>::nf && n <= STAGE - used) {
+            staged |= 1 << k;
             used += n;
         }
-        // forward caching reads the list once; a staged anchor list too
-        if (Shape<QT>::cached[f] || (staged >> f & 1)) tl.read(g.fwd.nbr + r.x, 4 * n);
     }
-    q[6] = staged;
+    if (f == 0) q[6] = staged;
     if constexpr (T::on) {
-        stats[4 * (int64_t)b] = (int64_t)tl.b;
-        stats[4 * (int64_t)b + 1] = (int64_t)tl.l;
+        // forward caching reads the list once; a staged anchor list too
+        if (f < Shape<QT>::nf && (Shape<QT>::cached[f] || (staged >> f & 1)))
+            tl.read(g.fwd.nbr + r.x, 4 * (r.y - r.x));
+        uint64_t x = tl.b, y = tl.l;
+        x += __shfl_xor(x, 1);
+        y += __shfl_xor(y, 1);
+        x += __shfl_xor(x, 2);
+        y += __shfl_xor(y, 2);
+        if (f == 0) {
+            stats[4 * (int64_t)b] = (int64_t)x;
+            stats[4 * (int64_t)b + 1] = (int64_t)y;
+        }
     }
 }
 
@@ -1255,45 +1279,53 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out
 constexpr int CK = 16;
 constexpr int CWAVES = 4;
 
+// One wavefront per listed query; its draws and states are read in one
+// round trip (the first round lists every query in order, so the list
+// itself is not read then, and the query's validity flag is loaded beside
+// the draws rather than before them).
 template <int NK>
 __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smore_sample_out out,
                                                              Ws ws, int cur, int32_t j_end, int last,
-                                                             int32_t tcap, int tshift)
+                                                             int32_t tcap, int tshift, int ident)
 {
     extern __shared__ int32_t lds[];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    int32_t* tv = lds + (size_t)w * 2 * tcap;
-    int32_t* tj = tv + tcap;
+    int32_t* tv = lds + (size_t)w * tcap;
     const uint64_t below = lanes_below(lane);
     const uint32_t tmask = (uint32_t)tcap - 1;
     const int32_t nact = uni(ws.ctrl[2 + cur]);
     if (blockIdx.x == 0 && threadIdx.x == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
     const int32_t nk = uni((j_end + 63) >> 6);
     for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
-        const int32_t b = uni(ws.act[cur][qi]);
-        if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
+        const int32_t b = ident ? qi : uni(ws.act[cur][qi]);
+        const int32_t flag = ws.qf[(int64_t)b * QF + 6];   // < 0: query without a valid positive
         const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
         int32_t c[NK];
-        bool non[NK];
+        uint8_t st[NK];
 #pragma unroll
         for (int k = 0; k < NK; ++k) {
             const int32_t j = 64 * k + lane;
             c[k] = -1;
-            non[k] = false;
+            st[k] = ST_ANS;
             if (k < nk && j < j_end) {
                 c[k] = cv[j];
-                non[k] = sv[j] == ST_NON;
+                st[k] = sv[j];
             }
         }
+        if (uni(flag) < 0) continue;
+        bool non[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) non[k] = st[k] == ST_NON;
         int4* t4 = (int4*)tv;
-        for (int32_t k = lane; k < tcap / 4; k += 64) {
-            t4[k] = make_int4(-1, -1, -1, -1);
-            ((int4*)tj)[k] = make_int4(INT_MAX, INT_MAX, INT_MAX, INT_MAX);
-        }
+        for (int32_t k = lane; k < tcap / 4; k += 64) t4[k] = make_int4(-1, -1, -1, -1);
         wave_sync();
-        // first probes of every draw in flight together; collisions probe on
+        // insert every non-answer's value; first probes of every draw in
+        // flight together, collisions probe on.  A draw that meets its own
+        // value in the table has an equal draw (which of the two came first
+        // is settled below); slots are never emptied, so two equal values
+        // always end in the same slot and one of them meets the other.
         uint32_t h[NK];
         int32_t old[NK];
 #pragma unroll
@@ -1301,6 +1333,7 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
             h[k] = ((uint32_t)c[k] * 0x9E3779B1u) >> tshift;
             old[k] = non[k] ? atomicCAS(&tv[h[k]], -1, c[k]) : -1;
         }
+        bool dup = false;
 #pragma unroll
         for (int k = 0; k < NK; ++k) {
             if (!non[k]) continue;
@@ -1311,12 +1344,26 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
                 o = atomicCAS(&tv[at], -1, c[k]);
             }
             h[k] = at;
-            atomicMin(&tj[at], 64 * k + lane);
+            dup = dup || o == c[k];
         }
-        wave_sync();
         int32_t first[NK];
 #pragma unroll
-        for (int k = 0; k < NK; ++k) first[k] = non[k] ? tj[h[k]] : -1;
+        for (int k = 0; k < NK; ++k) first[k] = non[k] ? 64 * k + lane : -1;
+        if (__ballot(dup)) {
+            // some value was drawn twice (rare): the first draw of each
+            // value is the least draw index over its slot (one slot per
+            // value, reused for the minimum)
+#pragma unroll
+            for (int k = 0; k < NK; ++k)
+                if (non[k]) tv[h[k]] = INT_MAX;
+            wave_sync();
+#pragma unroll
+            for (int k = 0; k < NK; ++k)
+                if (non[k]) atomicMin(&tv[h[k]], 64 * k + lane);
+            wave_sync();
+#pragma unroll
+            for (int k = 0; k < NK; ++k) first[k] = non[k] ? tv[h[k]] : -1;
+        }
         int32_t acc = 0;
 #pragma unroll
         for (int k = 0; k < NK; ++k) {
@@ -1383,7 +1430,7 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                   int64_t* stats, int32_t R, hipStream_t st, const char** err)
 {
     int rc;
-    k_prepare<QT, T><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, out, ws, stats, R);
+    k_prepare<QT, T><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, out, ws, stats, R);
     if ((rc = check_launch(err))) return rc;
     if (p.n_neg == 0) return SMORE_OK;
     const int rounds = n_rounds(p);
@@ -1402,23 +1449,27 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
         prof_mark(1, r, true, st);
-        const int32_t tcap = compact_tcap(j_end);
-        int tshift = 32;
-        for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
         if (j_end <= 64 * CK) {
+            // value table only, at load factor at most 0.3 (short probe chains)
+            const int32_t tcap = compact_tcap(2 * j_end);
+            int tshift = 32;
+            for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
             prof_mark(2, r, false, st);
-            const size_t tab = (size_t)CWAVES * 2 * tcap * sizeof(int32_t);
+            const size_t tab = (size_t)CWAVES * tcap * sizeof(int32_t);
             if (j_end <= 64 * 9)
                 k_compact_reg<9><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
-                                                                          r == rounds - 1, tcap, tshift);
+                                                                 r == rounds - 1, tcap, tshift, r == 0);
             else
                 k_compact_reg<CK><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
-                                                                           r == rounds - 1, tcap, tshift);
+                                                                  r == rounds - 1, tcap, tshift, r == 0);
             if ((rc = check_launch(err))) return rc;
             prof_mark(2, r, true, st);
             prev = j_end;
             continue;
         }
+        const int32_t tcap = compact_tcap(j_end);
+        int tshift = 32;
+        for (int32_t x = tcap; x > 1; x >>= 1) --tshift;
         const size_t lds = compact_lds(j_end);
         static bool attr = false;
         if (lds > 65536 && !attr) {
@@ -1564,7 +1615,7 @@ int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out
               uint32_t* mask, int32_t R, hipStream_t st, const char** err)
 {
     int rc;
-    k_prepare<QT, NoTally><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, q, ws, nullptr, R);
+    k_prepare<QT, NoTally><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, q, ws, nullptr, R);
     if ((rc = check_launch(err))) return rc;
     if (p.n_neg == 0) return SMORE_OK;
     k_candidates<QT, NoTally, true><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
