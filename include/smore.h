@@ -120,7 +120,9 @@ int smore_graph_info(const smore_graph *g, int64_t *n_entities, int64_t *n_relat
    (relation, first edge) pairs, 2 fwd neighbours [E], 3 rev node_ptr,
    4 rev groups, 5 rev neighbours, 6 active_in (entities with an in-edge,
    ascending), 7 in-edge mask [(V+31)/32] (bit v % 32 of word v / 32 set
-   iff entity v has an in-edge).  count must equal the array length.
+   iff entity v has an in-edge), 8 coarse in-edge mask [(V+127)/128] (bit
+   i % 32 of word i / 32 set iff one of entities 4i .. 4i+3 has an in-edge).
+   count must equal the array length.
    Synchronous. */
 int smore_graph_copy(const smore_graph *g, int32_t which, int32_t *host_dst, int64_t count);
 

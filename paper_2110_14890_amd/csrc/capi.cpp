@@ -366,6 +366,7 @@ int smore_graph_copy(const smore_graph* g, int32_t which, int32_t* host_dst, int
         case 5: src = g->r_nbr; n = g->E; break;
         case 6: src = g->active_in; n = g->n_active; break;
         case 7: src = g->has_in; n = ((int64_t)g->V + 31) / 32; break;
+        case 8: src = g->has_in4; n = ((int64_t)g->V + 127) / 128; break;
         default: return fail(SMORE_E_INVALID_ARG, "unknown array %d", which);
     }
     if (count != n) return fail(SMORE_E_INVALID_ARG, "array %d has %lld entries, not %lld", which,
@@ -404,7 +405,7 @@ void smore_free_graph(smore_graph* g)
     (void)hipGetDevice(&cur);
     if (cur != g->device) (void)hipSetDevice(g->device);
     void* bufs[] = {g->f_node, g->f_grp, g->f_nbr, g->r_node, g->r_grp, g->r_nbr, g->active_in,
-                    g->has_in};
+                    g->has_in, g->has_in4};
     for (void* b : bufs)
         if (b) (void)hipFree(b);
     if (cur >= 0 && cur != g->device) (void)hipSetDevice(cur);

@@ -250,6 +250,21 @@ __global__ void k_has_in(const int32_t* __restrict__ node, int32_t V, uint32_t* 
     bits[w] = word;
 }
 
+// bit i of the coarse mask: one of entities 4i .. 4i + 3 has an in-edge
+// (word w covers fine words 4w .. 4w + 3, eight bits from each)
+__global__ void k_has_in4(const uint32_t* __restrict__ bits, int64_t words, uint32_t* __restrict__ coarse)
+{
+    const int64_t w = (int64_t)blockIdx.x * BT + threadIdx.x;
+    if (w * 4 >= words) return;
+    uint32_t out = 0;
+    for (int f = 0; f < 4; ++f) {
+        const uint32_t x = w * 4 + f < words ? bits[w * 4 + f] : 0u;
+        for (int n = 0; n < 8; ++n)
+            if ((x >> (4 * n)) & 0xFu) out |= 1u << (8 * f + n);
+    }
+    coarse[w] = out;
+}
+
 inline unsigned grid_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // Owns temporary device buffers for the duration of a build.
@@ -493,9 +508,13 @@ int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_
     TRY(hipMalloc(&g->has_in, (size_t)words * 4));
     k_has_in<<<grid_for(words, BT), BT>>>(g->r_node, V, g->has_in);
     TRY(hipGetLastError());
+    const int64_t cwords = ((int64_t)V + 127) / 128;
+    TRY(hipMalloc(&g->has_in4, (size_t)cwords * 4));
+    k_has_in4<<<grid_for(cwords, BT), BT>>>(g->has_in, words, g->has_in4);
+    TRY(hipGetLastError());
     TRY(hipDeviceSynchronize());
     g->n_active = na;
-    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na + words) * 4 +
+    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na + words + cwords) * 4 +
                (size_t)(g->S_fwd + g->S_rev + 2) * sizeof(int2);
     return SMORE_OK;
 }

@@ -1042,8 +1042,12 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             // Every answer of every shape is reached by a projection, so a
             // draw without an in-edge is a non-answer: the in-edge mask (V
             // bits, resident in the last-level cache) decides most draws.
+            // On a large graph the coarse mask (one bit per four entities,
+            // small enough for the L2) is read first, and only draws whose
+            // group of four has an in-edge read the fine mask.
             int32_t c[DPW];
             uint32_t word[DPW];
+            const bool two_level = !use_lists && g.coarse;
 #pragma unroll
             for (int k = 0; k < DPW; ++k) {
                 const int32_t j = base + k * 64 + lane;
@@ -1057,7 +1061,18 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                         c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j),
                                                      (uint32_t)g.V);
                     }
-                    if (!use_lists && c[k] >= 0) word[k] = g.has_in[c[k] >> 5];
+                    if (!use_lists && c[k] >= 0)
+                        word[k] = two_level ? g.has_in4[c[k] >> 7] : g.has_in[c[k] >> 5];
+                }
+            }
+            if (two_level) {
+#pragma unroll
+                for (int k = 0; k < DPW; ++k) {
+                    const bool live = base + k * 64 + lane < j1 && c[k] >= 0;
+                    const bool maybe = live && ((word[k] >> ((c[k] >> 2) & 31)) & 1u);
+                    if (live) tl.read(g.has_in4 + (c[k] >> 7), 4);
+                    word[k] = maybe ? g.has_in[c[k] >> 5] : 0u;
+                    if (maybe) tl.read(g.has_in + (c[k] >> 5), 4);
                 }
             }
             if (use_lists) {
@@ -1081,7 +1096,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 const bool live = j < j1;
                 const bool in = live && c[k] >= 0 && ((word[k] >> (c[k] & 31)) & 1u);
                 if (live) {
-                    if (!use_lists && c[k] >= 0) tl.read(g.has_in + (c[k] >> 5), 4);
+                    if (!use_lists && !two_level && c[k] >= 0) tl.read(g.has_in + (c[k] >> 5), 4);
                     cv[j] = c[k];
                     if (!in) sv[j] = c[k] >= 0 ? ST_NON : ST_DUP;   // ST_DUP: not an entity
                 }
@@ -1657,6 +1672,10 @@ GraphView view_of(const smore_graph* g)
     gv.rev = DirView{g->r_node, g->r_grp, g->r_nbr};
     gv.active_in = g->active_in;
     gv.has_in = g->has_in;
+    gv.has_in4 = g->has_in4;
+    // above 2 MiB of fine mask (V > 2^24) the coarse mask (a quarter of
+    // the size) answers most draws from the L2
+    gv.coarse = g->V > (1 << 24);
     gv.V = g->V;
     gv.n_active = (int32_t)g->n_active;
     return gv;

@@ -24,6 +24,8 @@ struct GraphView {
     DirView fwd, rev;
     const int32_t* active_in;  // entities with an in-edge, ascending
     const uint32_t* has_in;    // bit v: entity v has an in-edge (V bits, cache-resident)
+    const uint32_t* has_in4;   // bit i: one of entities 4i .. 4i + 3 has an in-edge (V / 4 bits)
+    int32_t coarse;            // test has_in4 before has_in (when has_in outgrows the L2)
     int32_t V;
     int32_t n_active;
 };
@@ -85,7 +87,7 @@ struct smore_graph {
     int64_t E, S_fwd, S_rev, n_active;
     int32_t *f_node, *f_nbr, *r_node, *r_nbr, *active_in;
     int2 *f_grp, *r_grp;
-    uint32_t* has_in;
+    uint32_t *has_in, *has_in4;
     size_t bytes;
 };
 

@@ -44,6 +44,10 @@ def check_graph(g, og):
     words = g.copy(7, (g.V + 31) // 32).view(np.uint32)
     bits = np.unpackbits(words.view(np.uint8), bitorder="little")[:g.V]
     assert np.array_equal(np.nonzero(bits)[0], og.active_in())
+    # coarse mask: bit i iff one of entities 4i .. 4i + 3 has an in-edge
+    cw = g.copy(8, (g.V + 127) // 128).view(np.uint32)
+    cbits = np.unpackbits(cw.view(np.uint8), bitorder="little")
+    assert np.array_equal(np.nonzero(cbits)[0], np.unique(og.active_in() // 4))
 
 
 @pytest.mark.parametrize("case", ["dups", "dups_inverse", "tiny", "fb15k237", "fb400k", "empty",
@@ -134,6 +138,25 @@ def test_graph_without_in_edges_of_depth():
     ref = og.sample("2p", 4, 2)
     assert_same(got, ref, what="empty graph")
     assert (got["n_valid"] == -1).all()
+
+
+@pytest.mark.parametrize("qt", sm.TYPES)
+def test_two_level_in_edge_mask(qt):
+    # more than 2^24 entities: the candidate kernel tests the coarse mask
+    # (one bit per four entities) before the fine one; 100,000 entities
+    # scattered over 20,000,000 ids hold every edge
+    rng = np.random.default_rng(17)
+    V = 20_000_000
+    ents = rng.choice(V, 100_000, replace=False).astype(np.int32)
+    tr = np.stack([ents[rng.integers(0, len(ents), 400_000)], rng.integers(0, 8, 400_000),
+                   ents[rng.integers(0, len(ents), 400_000)]], axis=1).astype(np.int32)
+    g, og = graph_pair(tr, V, 8)
+    for n_neg, nt in [(64, 256), (600, 2400)]:
+        progress(f"two-level mask {qt} n_neg {n_neg}")
+        got = gpu_sample(g, qt, 512, n_neg, seed=5, neg_tries=nt)
+        ref = og.sample(qt, 512, n_neg, seed=5, neg_tries=nt)
+        assert_same(got, ref, what=f"{qt} n_neg {n_neg}")
+        assert (got["n_valid"] >= 0).mean() > 0.5
 
 
 def test_split_batch_and_repeat_are_identical():
