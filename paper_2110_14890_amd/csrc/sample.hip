@@ -1068,11 +1068,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             if (two_level) {
 #pragma unroll
                 for (int k = 0; k < DPW; ++k) {
+                    // accounted as one mask line per draw, as the one-level test
                     const bool live = base + k * 64 + lane < j1 && c[k] >= 0;
                     const bool maybe = live && ((word[k] >> ((c[k] >> 2) & 31)) & 1u);
                     if (live) tl.read(g.has_in4 + (c[k] >> 7), 4);
                     word[k] = maybe ? g.has_in[c[k] >> 5] : 0u;
-                    if (maybe) tl.read(g.has_in + (c[k] >> 5), 4);
                 }
             }
             if (use_lists) {
