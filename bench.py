@@ -239,6 +239,10 @@ def main():
     ap.add_argument("--c-sweep", action="store_true",
                     help="instead of the benchmark: minibatch time vs max expansion C, "
                          "GPU vs the exhaustive CPU oracle (2p, ip, pni)")
+    ap.add_argument("--serial", action="store_true",
+                    help="run the shapes of a step one after another on one stream "
+                         "(default: one stream per shape; a shape's negatives start when the "
+                         "previous shape's candidate kernel ends)")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -312,27 +316,46 @@ def main():
                     "draws": int(outs[qt]["neg_draws"].clamp(min=0).sum().item())}
         log(f"{qt}: {acct[qt]}")
 
-    def step(ev=None):
-        for qt in types:
-            if ev is not None:
-                ev[qt][0].record(stream)
-            sm.sample_positives(g, dags[qt], argv[qt], outs[qt], stream)
-            if ev is not None:
-                ev[qt][1].record(stream)
-                sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
-            sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, stream)
-            if ev is not None:
-                ev[qt][2].record(stream)
+    # one stream per shape (default priority, a workspace each).  Positives
+    # start together; a shape's negatives start when the previous shape's
+    # candidate kernel has ended (the event the library records after it),
+    # so each candidate kernel has the GPU mostly to itself while the
+    # long-list and selection kernels of the shape before it drain.
+    streams = {qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
+    go = torch.cuda.Event()
+    done = {qt: torch.cuda.Event() for qt in types}
 
+    def step(ev):
+        go.record(stream)
+        prev = None
+        for qt in types:
+            s = streams[qt]
+            if s is not stream:
+                s.wait_event(go)
+            ev[qt][0].record(s)
+            sm.sample_positives(g, dags[qt], argv[qt], outs[qt], s)
+            ev[qt][1].record(s)
+            if prev is not None and s is not stream:
+                s.wait_event(ev[prev][4])
+            sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
+            sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s)
+            ev[qt][2].record(s)
+            prev = qt
+        for qt in types:
+            if streams[qt] is not stream:
+                done[qt].record(streams[qt])
+                stream.wait_event(done[qt])
+
+    warm = {qt: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for qt in types}
     for _ in range(args.warmup):
-        step()
+        step(warm)
     torch.cuda.synchronize()
     evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for qt in types}
            for _ in range(args.steps)]
     for e in evs:                       # create the HIP events before the timed region
         for qt in types:
             for x in e[qt]:
-                x.record(stream)
+                x.record(streams[qt])
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -378,6 +401,10 @@ def main():
                 "bytes_per_launch": acct[dom]["cand_lines"] * 64,
                 "useful_bytes_per_launch": acct[dom]["cand_bytes"],
                 "avg_launch_ms": round(d["candidate_kernel_ms"], 4),
+                "launch_timing": ("HIP events around the launch on its stream, one stream for the step"
+                                  if args.serial else
+                                  "HIP events around the launch on its shape's stream; the long-list "
+                                  "and selection kernels of the previous shape may still be running"),
                 "accounting": "64-byte lines of graph data per dependent read of the candidate "
                               "kernel (in-edge mask word, reverse node pointers, relation-search "
                               "probes, group bounds, short backward lists, forward lists staged "
@@ -398,7 +425,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload_name(cfg, types), "types": types, "batch": cfg.batch,
                    "n_neg": cfg.n_neg, "neg_tries": neg_tries, "pos_tries": 64,
-                   "seed": cfg.seed, "graph_seed": cfg.graph_seed},
+                   "seed": cfg.seed, "graph_seed": cfg.graph_seed,
+                   "streams": 1 if args.serial else len(types)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "gather_ceiling": ceiling,

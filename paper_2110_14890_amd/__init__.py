@@ -211,11 +211,14 @@ class Workspace:
 _default_ws = {}
 
 
-def _workspace(ws, dag, args):
+def _workspace(ws, dag, args, stream=None):
+    """The caller's workspace, or a default one per (device, stream) the call
+    runs on, so that calls on different streams never share scratch."""
     import torch
     if ws is None:
-        key = (torch.cuda.current_device(), torch.cuda.current_stream().cuda_stream)
-        ws = _default_ws.setdefault(key, Workspace())
+        st = stream if stream is not None else torch.cuda.current_stream()
+        key = (st.device, st.cuda_stream)
+        ws = _default_ws.setdefault(key, Workspace(st.device))
     buf = ws.get(workspace_bytes(dag, args))
     return c_vp(buf.data_ptr()), buf.numel()
 
@@ -223,7 +226,7 @@ def _workspace(ws, dag, args):
 def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
                 workspace: "Workspace | None" = None) -> dict:
     """smore_sample into caller-owned torch tensors on the current (or given) stream."""
-    wp, wn = _workspace(workspace, dag, args)
+    wp, wn = _workspace(workspace, dag, args, stream)
     _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                               ctypes.byref(_out_struct(out)), wp, wn, _stream_handle(stream)))
     return out
@@ -243,7 +246,7 @@ def alloc_shared_outputs(batch: int, n_shared: int, device=None) -> dict:
 def sample_shared_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
                        workspace: "Workspace | None" = None) -> dict:
     """smore_sample_shared: args.n_neg is the size of the shared candidate set."""
-    wp, wn = _workspace(workspace, dag, args)
+    wp, wn = _workspace(workspace, dag, args, stream)
     st = SharedOut(*[out[k].data_ptr() if out[k].numel() else None for k in SHARED_FIELDS])
     _check(lib().smore_sample_shared(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                                      ctypes.byref(st), wp, wn, _stream_handle(stream)))
@@ -278,7 +281,7 @@ def verify(graph: Graph, qtype: "str | QueryDag", anchors, relations, candidates
     dev = candidates.device
     out = {"mask": torch.empty((batch, (n + 31) // 32), dtype=torch.int32, device=dev),
            "n_valid": torch.empty(batch, dtype=torch.int32, device=dev)}
-    wp, wn = _workspace(workspace, dag, args)
+    wp, wn = _workspace(workspace, dag, args, stream)
     ptr = lambda t: t.data_ptr() if t.numel() else None
     _check(lib().smore_verify(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                               anchors.data_ptr(), relations.data_ptr(), ptr(candidates),
@@ -314,7 +317,7 @@ def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, s
     graph data read per query by the candidate kernel, then by the kernel
     that intersects long lists."""
     sp = c_vp(stats.data_ptr()) if stats is not None else None
-    wp, wn = _workspace(workspace, dag, args)
+    wp, wn = _workspace(workspace, dag, args, stream)
     _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                                         ctypes.byref(_out_struct(out)), sp, wp, wn,
                                         _stream_handle(stream)))

@@ -180,6 +180,24 @@ def test_split_batch_and_repeat_are_identical():
             assert np.array_equal(full[k], out[k].cpu().numpy())
 
 
+def test_concurrent_streams_give_the_same_rows():
+    # three shapes at once, one stream each, default workspaces (one per
+    # stream): the rows equal those of one stream
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    types = ("3p", "ip", "pni")
+    ref = {qt: gpu_sample(g, qt, 512, 128, seed=2) for qt in types}
+    streams = {qt: torch.cuda.Stream() for qt in types}
+    for rep in range(3):
+        outs = {qt: sm.sample(g, qt, 512, 128, seed=2, stream=streams[qt]) for qt in types}
+        torch.cuda.synchronize()
+        for qt in types:
+            got = to_numpy(outs[qt])
+            for k in ref[qt]:
+                assert np.array_equal(got[k], ref[qt][k]), (rep, qt, k)
+
+
 def test_plan_outside_the_presets_is_refused_on_device_graph():
     # a complement at the root (not one of the fourteen structures)
     g = sm.Graph(np.array([[0, 0, 1]], np.int32), 2, 1)
