@@ -316,41 +316,53 @@ def main():
                     "draws": int(outs[qt]["neg_draws"].clamp(min=0).sum().item())}
         log(f"{qt}: {acct[qt]}")
 
-    # one stream per shape (default priority, a workspace each).  Positives
-    # start together; a shape's negatives start when the previous shape's
-    # candidate kernel has ended (the event the library records after it),
-    # so each candidate kernel has the GPU mostly to itself while the
-    # long-list and selection kernels of the shape before it drain.
+    # One stream per shape (default priority, a workspace each); each stream
+    # runs its shape's steps in order.  The candidate kernels of all shapes
+    # and steps form one chain (3p, ip, pi, the next step's 3p, ...): a
+    # shape's negatives start when the candidate kernel before it in the
+    # chain has ended (the event the library records after that kernel), so
+    # each candidate kernel has the GPU mostly to itself while positives and
+    # the long-list and selection kernels of other shapes run beside it.
+    # The streams join the timing stream only at the ends of the timed region.
     streams = {qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
-    go = torch.cuda.Event()
-    done = {qt: torch.cuda.Event() for qt in types}
+    join = {qt: torch.cuda.Event() for qt in types}
+    chain = [None]   # end event of the last candidate kernel launched
+
+    def fork():
+        join["fork"] = torch.cuda.Event()
+        join["fork"].record(stream)
+        for qt in types:
+            if streams[qt] is not stream:
+                streams[qt].wait_event(join["fork"])
+
+    def merge():
+        for qt in types:
+            if streams[qt] is not stream:
+                join[qt].record(streams[qt])
+                stream.wait_event(join[qt])
+        chain[0] = None
 
     def step(ev):
-        go.record(stream)
-        prev = None
         for qt in types:
             s = streams[qt]
-            if s is not stream:
-                s.wait_event(go)
             ev[qt][0].record(s)
             sm.sample_positives(g, dags[qt], argv[qt], outs[qt], s)
             ev[qt][1].record(s)
-            if prev is not None and s is not stream:
-                s.wait_event(ev[prev][4])
+            if chain[0] is not None and s is not stream:
+                s.wait_event(chain[0])
+            ev[qt][5].record(s)   # the negative stage starts here, after the wait
             sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
             sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s)
             ev[qt][2].record(s)
-            prev = qt
-        for qt in types:
-            if streams[qt] is not stream:
-                done[qt].record(streams[qt])
-                stream.wait_event(done[qt])
+            chain[0] = ev[qt][4]
 
-    warm = {qt: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for qt in types}
+    warm = {qt: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for qt in types}
+    fork()
     for _ in range(args.warmup):
         step(warm)
+    merge()
     torch.cuda.synchronize()
-    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for qt in types}
+    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for qt in types}
            for _ in range(args.steps)]
     for e in evs:                       # create the HIP events before the timed region
         for qt in types:
@@ -361,8 +373,10 @@ def main():
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
+    fork()
     for k in range(args.steps):
         step(evs[k])
+    merge()
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
@@ -370,7 +384,7 @@ def main():
     per_type = {}
     for qt in types:
         pos = float(np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs]))
-        neg = float(np.mean([e[qt][1].elapsed_time(e[qt][2]) for e in evs]))
+        neg = float(np.mean([e[qt][5].elapsed_time(e[qt][2]) for e in evs]))
         cand = float(np.mean([e[qt][3].elapsed_time(e[qt][4]) for e in evs]))
         a = acct[qt]
         per_type[qt] = {
@@ -403,8 +417,8 @@ def main():
                 "avg_launch_ms": round(d["candidate_kernel_ms"], 4),
                 "launch_timing": ("HIP events around the launch on its stream, one stream for the step"
                                   if args.serial else
-                                  "HIP events around the launch on its shape's stream; the long-list "
-                                  "and selection kernels of the previous shape may still be running"),
+                                  "HIP events around the launch on its shape's stream; positives and the "
+                                  "long-list and selection kernels of other shapes may run beside it"),
                 "accounting": "64-byte lines of graph data per dependent read of the candidate "
                               "kernel (in-edge mask word, reverse node pointers, relation-search "
                               "probes, group bounds, short backward lists, forward lists staged "
