@@ -343,11 +343,13 @@ def main():
         chain[0] = None
 
     def step(ev):
-        for qt in types:
+        for qt in types:   # positives first: they wait for nothing but their own stream
             s = streams[qt]
             ev[qt][0].record(s)
             sm.sample_positives(g, dags[qt], argv[qt], outs[qt], s)
             ev[qt][1].record(s)
+        for qt in types:
+            s = streams[qt]
             if chain[0] is not None and s is not stream:
                 s.wait_event(chain[0])
             ev[qt][5].record(s)   # the negative stage starts here, after the wait
@@ -373,14 +375,17 @@ def main():
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
+    h0 = time.perf_counter()
     fork()
     for k in range(args.steps):
         step(evs[k])
     merge()
     t_end.record(stream)
+    host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
+    log(f"host enqueue {host_ms:.3f} ms per step, device {ms_step:.3f} ms per step")
     per_type = {}
     for qt in types:
         pos = float(np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs]))
