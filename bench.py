@@ -192,6 +192,61 @@ def shared_bench(cfg, g, types, steps, warmup, stream):
               flush=True)
 
 
+def verify_bench(cfg, g, types, steps, warmup, stream):
+    """Evaluation-time work on the workload's graph (appendix on the task
+    setup and the metrics): for each shape, the batch's queries (positives
+    only) with 1,000 uniform candidates each are verified by smore_verify
+    (membership of every (query, candidate) pair), and smore_sample draws
+    1,000 filtered negatives per query.  One JSON line per shape."""
+    import torch
+
+    import paper_2110_14890_amd as sm
+
+    n_cand = 1000
+    for qt in types:
+        dag = sm.query_preset(qt)
+        args = sm.make_args(cfg.batch, 0, seed=cfg.seed)
+        q = sm.alloc_outputs(cfg.batch, 0)
+        sm.sample_positives(g, dag, args, q, stream)
+        gen = torch.Generator(device="cuda").manual_seed(cfg.seed)
+        cand = torch.randint(0, cfg.n_entities, (cfg.batch, n_cand), generator=gen, device="cuda",
+                             dtype=torch.int64).to(torch.int32)
+        torch.cuda.synchronize()
+        ws = sm.Workspace()
+        for _ in range(warmup):
+            sm.verify(g, dag, q["anchors"], q["relations"], cand, stream=stream, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            out = sm.verify(g, dag, q["anchors"], q["relations"], cand, stream=stream, workspace=ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        vms = e0.elapsed_time(e1) / steps
+        valid = int((out["n_valid"] >= 0).sum().item())
+        # filtered evaluation negatives: 1,000 per query, up to 4,000 draws
+        eargs = sm.make_args(cfg.batch, n_cand, seed=cfg.seed, neg_tries=4 * n_cand)
+        eo = sm.alloc_outputs(cfg.batch, n_cand)
+        for _ in range(warmup):
+            sm.sample_into(g, dag, eargs, eo, stream, workspace=ws)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            sm.sample_into(g, dag, eargs, eo, stream, workspace=ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        sms = e0.elapsed_time(e1) / steps
+        nv = eo["n_valid"]
+        print(json.dumps({"mode": "evaluation", "shape": qt, "queries": cfg.batch,
+                          "verify_candidates_per_query": n_cand,
+                          "verify_ms": round(vms, 4),
+                          "verified_pairs_per_s": round(valid * n_cand / (vms / 1e3), 1),
+                          "filtered_negatives_per_query": n_cand,
+                          "sample_ms": round(sms, 4),
+                          "sample_queries_per_s": round(cfg.batch / (sms / 1e3), 1),
+                          "complete_queries": int((nv == n_cand).sum().item())}), flush=True)
+
+
 def cpu_baseline(cfg, triples, types, seconds, threads):
     """The CPU oracle, timed on the host on the first queries of each shape
     (a bounded sample of the same workload)."""
@@ -236,6 +291,9 @@ def main():
     ap.add_argument("--no-gather-ceiling", action="store_true")
     ap.add_argument("--shared", action="store_true",
                     help="instead of the benchmark: minibatches sharing one candidate set")
+    ap.add_argument("--verify", action="store_true",
+                    help="instead of the benchmark: evaluation-time verification of 1,000 "
+                         "candidates per query, and 1,000 filtered negatives per query")
     ap.add_argument("--c-sweep", action="store_true",
                     help="instead of the benchmark: minibatch time vs max expansion C, "
                          "GPU vs the exhaustive CPU oracle (2p, ip, pni)")
@@ -294,6 +352,9 @@ def main():
         return
     if args.shared:
         shared_bench(cfg, g, types, args.steps, args.warmup, stream)
+        return
+    if args.verify:
+        verify_bench(cfg, g, types, args.steps, args.warmup, stream)
         return
     neg_tries = 4 * cfg.n_neg
     dags = {qt: sm.query_preset(qt) for qt in types}
