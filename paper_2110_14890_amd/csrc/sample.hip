@@ -1008,7 +1008,8 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
     const int32_t nwaves = gridDim.x * (CWG / 64);
     T tl;
     for (int32_t qi = uni(blockIdx.x * (CWG / 64) + w); qi < nact; qi += nwaves) {
-        const int32_t b = uni(ws.act[cur][qi]);
+        // the first round lists every query in order: the list is not read
+        const int32_t b = j0 == 0 ? qi : uni(ws.act[cur][qi]);
         const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
         int32_t anc[3], rel[3];
         for (int k = 0; k < 3; ++k) {
@@ -1019,25 +1020,43 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
         const int32_t staged = uni(qb[6]);
         if (staged < 0) continue;   // query without a valid positive
         FSet F[3];
-        int32_t used = 0;
+        int32_t sbeg[3], used = 0;
 #pragma unroll
         for (int f = 0; f < 3; ++f) {
+            sbeg[f] = 0;
             if (f >= Shape<QT>::nf) { F[f] = FSet{nullptr, 0, true}; continue; }
             const int32_t beg = uni(qb[2 * f]), n = uni(qb[2 * f + 1]) - beg;
             if (staged >> f & 1) {
-                for (int32_t k = lane; k < n; k += 64) stage[used + k] = g.fwd.nbr[beg + k];
+                sbeg[f] = beg;
                 F[f] = FSet{stage + used, n, true};
                 used += n;
             } else {
                 F[f] = FSet{g.fwd.nbr + beg, n, false};
             }
         }
+        // copy of the staged lists into the wave's LDS slice
+        auto stage_lists = [&]() {
+#pragma unroll
+            for (int f = 0; f < 3; ++f) {
+                if (f >= Shape<QT>::nf || !(staged >> f & 1)) continue;
+                int32_t* dst = stage + (F[f].p - stage);
+                for (int32_t k = lane; k < F[f].n; k += 64) dst[k] = g.fwd.nbr[sbeg[f] + k];
+            }
+            wave_sync();
+        };
         int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         // first test of every draw: the staged root-edge lists when the
-        // shape has them (LDS only), else the in-edge mask
+        // shape has them (LDS only), else the in-edge mask; in the latter
+        // case the lists are copied while the first window's mask words
+        // are in flight
         constexpr int RM = RootLists<QT>::mask;
         const bool use_lists = RM != 0 && (RootLists<QT>::any ? (staged & RM) == RM : (staged & RM) != 0);
+        bool to_stage = used > 0;
+        if (use_lists) {
+            stage_lists();
+            to_stage = false;
+        }
         for (int32_t base = j0; base < j1; base += WIN) {
             // Every answer of every shape is reached by a projection, so a
             // draw without an in-edge is a non-answer: the in-edge mask (V
@@ -1064,6 +1083,10 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                     if (!use_lists && c[k] >= 0)
                         word[k] = two_level ? g.has_in4[c[k] >> 7] : g.has_in[c[k] >> 5];
                 }
+            }
+            if (to_stage) {
+                stage_lists();
+                to_stage = false;
             }
             if (two_level) {
 #pragma unroll
