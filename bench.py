@@ -301,6 +301,9 @@ def main():
                     help="run the shapes of a step one after another on one stream "
                          "(default: one stream per shape; a shape's negatives start when the "
                          "previous shape's candidate kernel ends)")
+    ap.add_argument("--prepare-ahead", action="store_true",
+                    help="with one stream per shape, let a shape's preparation run before the "
+                         "wait for the previous candidate kernel (smore_wait_before_kernel)")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -381,9 +384,11 @@ def main():
     # runs its shape's steps in order.  The candidate kernels of all shapes
     # and steps form one chain (3p, ip, pi, the next step's 3p, ...): a
     # shape's negatives start when the candidate kernel before it in the
-    # chain has ended (the event the library records after that kernel), so
-    # each candidate kernel has the GPU mostly to itself while positives and
-    # the long-list and selection kernels of other shapes run beside it.
+    # chain has ended (the event the library records after that kernel; with
+    # --prepare-ahead the library waits for it only after the shape's
+    # preparation), so each candidate kernel has the GPU mostly to itself
+    # while positives and the long-list and selection kernels of other
+    # shapes run beside it.
     # The streams join the timing stream only at the ends of the timed region.
     streams = {qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
     join = {qt: torch.cuda.Event() for qt in types}
@@ -412,8 +417,11 @@ def main():
         for qt in types:
             s = streams[qt]
             if chain[0] is not None and s is not stream:
-                s.wait_event(chain[0])
-            ev[qt][5].record(s)   # the negative stage starts here, after the wait
+                if args.prepare_ahead:
+                    sm.wait_before_kernel(chain[0])
+                else:
+                    s.wait_event(chain[0])
+            ev[qt][5].record(s)
             sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
             sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s)
             ev[qt][2].record(s)
@@ -453,9 +461,12 @@ def main():
         neg = float(np.mean([e[qt][5].elapsed_time(e[qt][2]) for e in evs]))
         cand = float(np.mean([e[qt][3].elapsed_time(e[qt][4]) for e in evs]))
         a = acct[qt]
+        # with --prepare-ahead the negative stage includes the wait for the
+        # previous shape's candidate kernel: no per-shape rates then
+        rated = not args.prepare_ahead
         per_type[qt] = {
-            "queries_per_s": cfg.batch / ((pos + neg) / 1e3),
-            "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3),
+            "queries_per_s": cfg.batch / ((pos + neg) / 1e3) if rated else None,
+            "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3) if rated else None,
             "positive_ms": pos, "negative_stage_ms": neg, "candidate_kernel_ms": cand,
             "candidate_kernel_line_GBps": a["cand_lines"] * 64 / (cand / 1e3) / 1e9,
             "candidate_kernel_useful_GBps": a["cand_bytes"] / (cand / 1e3) / 1e9,

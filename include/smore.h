@@ -263,6 +263,18 @@ int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_s
    caller.  Returns SMORE_E_INVALID_ARG for another `which`. */
 int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
 
+/* Scheduling, for callers that run several sampling calls on different
+   streams and want their candidate kernels one after another: the next
+   smore_sample or smore_sample_negatives call made by this thread makes its
+   stream wait on the caller's HIP event (hipEvent_t) right before its
+   first candidate kernel (which = 0), after the per-query preparation, so
+   the preparation does not wait.  One-shot: the next such call disarms it,
+   also when it launches no candidate kernel (n_neg = 0).  NULL disarms.
+   The event stays owned by the caller.  SMORE_E_INVALID_ARG for another
+   `which`; SMORE_E_HIP if the wait cannot be enqueued (the call then
+   launches nothing after the preparation). */
+int smore_wait_before_kernel(void *event, int32_t which);
+
 /* Instrumentation: n_reads random 4-byte reads from the device table of
    table_bytes (the first word of pseudo-randomly chosen 64-byte lines among
    the largest power-of-two number of lines that fits), eight independent

@@ -96,6 +96,7 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp, c_vp, ctypes.c_size_t, c_vp]
         L.smore_profile_kernel.argtypes = [c_vp, c_vp, c_i32]
+        L.smore_wait_before_kernel.argtypes = [c_vp, c_i32]
         L.smore_gather_probe.argtypes = [c_vp, c_i64, c_i64, c_vp, c_i64, c_vp]
         L.smore_free_graph.argtypes = [c_vp]
         L.smore_free_graph.restype = None
@@ -335,6 +336,18 @@ def profile_kernel(start_event, stop_event, which: int = KERNEL_CANDIDATES) -> N
             ev.record()
     _check(lib().smore_profile_kernel(c_vp(start_event.cuda_event), c_vp(stop_event.cuda_event),
                                       which))
+
+
+def wait_before_kernel(event, which: int = KERNEL_CANDIDATES) -> None:
+    """The next negatives call on this thread waits on the torch.cuda.Event
+    right before its first candidate kernel (smore_wait_before_kernel);
+    None disarms."""
+    if event is None:
+        _check(lib().smore_wait_before_kernel(None, which))
+        return
+    if not event.cuda_event:           # torch creates the HIP event on first use
+        event.record()
+    _check(lib().smore_wait_before_kernel(c_vp(event.cuda_event), which))
 
 
 def sample(graph: Graph, qtype: "str | QueryDag", batch: int, n_neg: int, seed: int = 0,

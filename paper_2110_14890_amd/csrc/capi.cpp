@@ -384,6 +384,13 @@ int smore_profile_kernel(void* start_event, void* stop_event, int32_t which)
     return ok();
 }
 
+int smore_wait_before_kernel(void* event, int32_t which)
+{
+    if (which != 0) return fail(SMORE_E_INVALID_ARG, "only the candidate kernel (which = 0) can wait");
+    smore::arm_wait(event);
+    return ok();
+}
+
 int smore_gather_probe(const void* table, int64_t table_bytes, int64_t n_reads, uint32_t* sink,
                        int64_t sink_words, void* hip_stream)
 {

@@ -1456,6 +1456,10 @@ struct ProfileArm {
 };
 thread_local ProfileArm g_prof;
 
+// One-shot wait of the next negatives call: its stream waits on this event
+// right before the first candidate kernel, after the preparation.
+thread_local hipEvent_t g_wait = nullptr;
+
 inline void prof_mark(int which, int round, bool after, hipStream_t st)
 {
     if (round != 0 || g_prof.which != which || !g_prof.start || !g_prof.stop) return;
@@ -1479,6 +1483,11 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         // later rounds carry the few queries short of n_neg: a smaller grid
         // keeps their (often empty) launches cheap
         const int grid = r == 0 ? PERSIST_BLOCKS : PERSIST_BLOCKS / 4;
+        if (r == 0 && g_wait) {
+            const hipError_t e = hipStreamWaitEvent(st, g_wait, 0);
+            g_wait = nullptr;
+            if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
+        }
         prof_mark(0, r, false, st);
         k_candidates<QT, T><<<grid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
         if ((rc = check_launch(err))) return rc;
@@ -1706,6 +1715,8 @@ GraphView view_of(const smore_graph* g)
 
 }  // namespace
 
+void arm_wait(void* event) { g_wait = (hipEvent_t)event; }
+
 void arm_profile(void* start_event, void* stop_event, int which)
 {
     g_prof.start = (hipEvent_t)start_event;
@@ -1741,6 +1752,7 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
     const int rc = stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, st, err)
                          : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
     g_prof = ProfileArm{};  // one-shot: an arm never outlives the call it was meant for
+    g_wait = nullptr;
     return rc;
 }
 

@@ -39,6 +39,12 @@ def declared_functions():
                                  re.M)))
 
 
+def test_wait_hook_validation_on_host(L):
+    # only the candidate kernel can wait; NULL disarms
+    assert L.smore_wait_before_kernel(None, 1) == -1
+    assert L.smore_wait_before_kernel(None, 0) == 0
+
+
 def test_exports_every_declared_function(L):
     names = declared_functions()
     assert len(names) >= 9

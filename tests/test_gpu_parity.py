@@ -198,6 +198,30 @@ def test_concurrent_streams_give_the_same_rows():
                 assert np.array_equal(got[k], ref[qt][k]), (rep, qt, k)
 
 
+def test_wait_before_candidates_keeps_rows():
+    # shape B's candidate kernel waits for an event recorded after shape A's
+    # sampling on another stream; rows equal the plain ones, and an unused
+    # arm (n_neg = 0) is dropped
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    ref = {qt: gpu_sample(g, qt, 512, 128, seed=4) for qt in ("3p", "pni")}
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    done = torch.cuda.Event()
+    a = sm.sample(g, "3p", 512, 128, seed=4, stream=sa)
+    done.record(sa)
+    sm.wait_before_kernel(done)
+    b = sm.sample(g, "pni", 512, 128, seed=4, stream=sb)
+    sm.wait_before_kernel(done)
+    sm.sample(g, "2p", 64, 0, stream=sb)
+    c = sm.sample(g, "pni", 512, 128, seed=4, stream=sb)
+    torch.cuda.synchronize()
+    for qt, out in (("3p", a), ("pni", b), ("pni", c)):
+        got = to_numpy(out)
+        for k in ref[qt]:
+            assert np.array_equal(got[k], ref[qt][k]), (qt, k)
+
+
 def test_plan_outside_the_presets_is_refused_on_device_graph():
     # a complement at the root (not one of the fourteen structures)
     g = sm.Graph(np.array([[0, 0, 1]], np.int32), 2, 1)
