@@ -159,6 +159,25 @@ def test_two_level_in_edge_mask(qt):
         assert (got["n_valid"] >= 0).mean() > 0.5
 
 
+def test_single_entity_graph_and_single_query():
+    # one entity with a self-loop: every draw is the one answer, so no
+    # negative exists and the budget runs out; shapes that need distinct
+    # siblings (or a negated operand that misses the root) find no positive
+    g, og = graph_pair(np.array([[0, 0, 0]], np.int32), 1, 1)
+    for qt in sm.TYPES:
+        got = gpu_sample(g, qt, 3, 2, seed=1, pos_tries=8, neg_tries=5)
+        ref = og.sample(qt, 3, 2, seed=1, pos_tries=8, neg_tries=5)
+        assert_same(got, ref, what=f"one entity {qt}")
+    # a batch of one query, at an offset next to the end of the id range
+    rng = np.random.default_rng(8)
+    tr = kgsynth.random_tiny(rng, 500, 4, 6000)
+    g, og = graph_pair(tr, 500, 4, True)
+    for qt in sm.TYPES:
+        got = gpu_sample(g, qt, 1, 40, seed=12, query_offset=2**32 - 1)
+        ref = og.sample(qt, 1, 40, seed=12, query_offset=2**32 - 1)
+        assert_same(got, ref, what=f"one query {qt}")
+
+
 def test_split_batch_and_repeat_are_identical():
     import torch
     cfg, tr = config_graph("fb15k237")
