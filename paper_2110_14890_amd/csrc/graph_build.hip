@@ -11,7 +11,9 @@
 //   4. a stable sort of the deduplicated records by r, then t, gives
 //      (t, r, h) order (the input is already ordered by h within (t, r));
 //      reverse groups and node pointers as in 3;
-//   5. active_in = entities whose reverse node range is non-empty.
+//   5. active_in = entities whose reverse node range is non-empty, the
+//      in-edge mask (one bit per entity) and the coarse mask (one bit per
+//      four entities) built from it.
 // One-time and synchronous; the sampler never calls it.
 #include <hip/hip_runtime.h>
 

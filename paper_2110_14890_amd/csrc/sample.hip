@@ -13,14 +13,21 @@
 //
 // Negatives (smore_sample_negatives): bidirectional rejection sampling
 // (Sec. 3.2) at the node cut the planner picks for the shape, in rounds of
-// candidate draws; k_prepare once, then per round k_candidates,
-// k_heavy and k_compact, all on the caller's stream with no host
-// synchronisation in between (the kernels themselves are described where
-// they are defined).  Forward caching turns the anchors into their
-// neighbour lists A_r(a) (sorted CSR groups, staged in LDS when small, used
-// in place when not); each draw is verified backward from the candidate;
-// the first occurrences of the non-answers, in draw order, are the
-// negatives, so the output is a function of the draw indices alone.
+// candidate draws; k_prepare once, then per round k_candidates, k_heavy
+// and the selection (k_compact_reg, or k_compact for long rounds), all on
+// the caller's stream with no host synchronisation in between (the kernels
+// themselves are described where they are defined).  Forward caching turns
+// the anchors into their neighbour lists A_r(a) (sorted CSR groups, staged
+// in LDS when small, used in place when not); a draw without an in-edge is
+// settled by the in-edge mask (on large graphs a coarse mask first); the
+// others are verified backward from the candidate; the first occurrences
+// of the non-answers, in draw order, are the negatives, so the output is a
+// function of the draw indices alone.
+//
+// Shared-candidate minibatches (smore_sample_shared) and verification of
+// caller candidates (smore_verify) run the same candidate and long-list
+// kernels on given candidates, then pack the states into mask rows
+// (k_shared_set, k_pack).
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -495,8 +502,9 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
 //                 level or a push to the heavy queue;
 //   k_heavy       one wavefront per queued (query, draw): intersection of a
 //                 long backward list with the forward-cached list(s);
-//   k_compact     one wavefront per query: first-occurrence test of every
-//                 draw so far, ordered selection of the first n_neg kept.
+//   k_compact_reg one wavefront per query (k_compact for rounds of more
+//                 than 1,024 draws): first-occurrence test of every draw so
+//                 far, ordered selection of the first n_neg kept.
 // Queries still short of n_neg after a round go to the next round through a
 // device-side list, so rounds need no host synchronisation.
 
