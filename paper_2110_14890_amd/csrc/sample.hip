@@ -393,8 +393,9 @@ __device__ bool neg_member(const GraphView& g, int steps, int32_t a, int32_t r0,
 // Attempts of one query run PA at a time, on PA neighbouring lanes (lane l
 // of the group takes attempts l, l + PA, ...): the lowest successful
 // attempt of a group step is the first successful attempt overall, so the
-// result is that of trying them one after the other.
-constexpr int PA = 4;
+// result is that of trying them one after the other.  Four lanes per query,
+// eight for plans with a complemented operand, whose attempts are rejected
+// more often.
 
 // One attempt t of query q: true and the grounded registers when accepted.
 __device__ __forceinline__ bool pos_attempt(const GraphView& g, const WalkProgram& wp,
@@ -452,6 +453,7 @@ __device__ __forceinline__ bool pos_attempt(const GraphView& g, const WalkProgra
     return true;
 }
 
+template <int PA>
 __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, SampleParams p,
                                                   smore_sample_out out)
 {
@@ -1740,9 +1742,11 @@ size_t negatives_workspace_bytes(const SampleParams& p)
 int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
                     const smore_sample_out& out, hipStream_t st, const char** err)
 {
-    static_assert(256 % PA == 0 && (PA & (PA - 1)) == 0, "attempt groups tile the workgroup");
-    const int64_t threads = (int64_t)p.batch * PA;
-    k_positive<<<(unsigned)((threads + 255) / 256), 256, 0, st>>>(view_of(g), wp, p, out);
+    const int pa = wp.neg_steps > 0 ? 8 : 4;   // attempt lanes per query (they divide 64)
+    const int64_t threads = (int64_t)p.batch * pa;
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    if (pa == 8) k_positive<8><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
+    else k_positive<4><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
     return check_launch(err);
 }
 
