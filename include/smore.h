@@ -34,7 +34,8 @@ enum {
     SMORE_E_UNSUPPORTED = -3, /* plan outside the fourteen shapes, limits */
     SMORE_E_NOMEM = -4,       /* device or host allocation failed */
     SMORE_E_HIP = -5,         /* a HIP runtime call failed */
-    SMORE_E_OVERFLOW = -6     /* counts beyond the int32 / 32-bit query-id range */
+    SMORE_E_OVERFLOW = -6     /* counts beyond the int32 / 32-bit query-id range, or
+                                 batch x neg_tries of 2^31 or more */
 };
 
 /* flags of smore_build_graph */

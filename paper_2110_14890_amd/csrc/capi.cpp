@@ -463,6 +463,9 @@ int check_args(const smore_query_dag* dag, const smore_sample_args* a, int* qt_o
     if (a->flags != 0) return fail(SMORE_E_INVALID_ARG, "flags must be 0");
     if (a->query_offset > (1ull << 32) || a->query_offset + (uint64_t)a->batch > (1ull << 32))
         return fail(SMORE_E_OVERFLOW, "query ids must stay below 2^32");
+    // the long-list queue is indexed by a 32-bit counter over batch x round length
+    if ((int64_t)a->batch * a->neg_tries >= ((int64_t)1 << 31))
+        return fail(SMORE_E_OVERFLOW, "batch x neg_tries must stay below 2^31");
     *qt_out = qt;
     return SMORE_OK;
 }

@@ -198,6 +198,8 @@ def test_sample_validation_on_host(L):
         a = sm.make_args(4, 2)
         setattr(a, field, val)
         _expect(_call_sample(L, dag, a, ptrs), code)
+    big = sm.make_args(2**20, 2048)                                # batch x neg_tries = 2^31
+    _expect(_call_sample(L, dag, big, ptrs), -6)
     _expect(_call_sample(L, dag, good, ptrs[:3] + [None] + ptrs[4:]), -1)   # negatives NULL
     a0 = sm.make_args(4, 0)
     _call_sample(L, dag, a0, ptrs[:3] + [None] + ptrs[4:])
@@ -205,7 +207,7 @@ def test_sample_validation_on_host(L):
     neg = sm.QueryDag.from_buffer_copy(dag)
     neg.node[2].op = sm.OP_NOT
     neg.node[2].slot = -1
-    _expect(_call_sample(L, neg, good, ptrs), -3)                 # negation
+    _expect(_call_sample(L, neg, good, ptrs), -3)                 # not a preset
     other = sm.QueryDag.from_buffer_copy(sm.query_preset("2i"))
     other.node[4].child[0], other.node[4].child[1] = 3, 1         # same tree, other order
     _expect(_call_sample(L, other, good, ptrs), -3)
