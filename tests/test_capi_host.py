@@ -198,7 +198,7 @@ def test_sample_validation_on_host(L):
         a = sm.make_args(4, 2)
         setattr(a, field, val)
         _expect(_call_sample(L, dag, a, ptrs), code)
-    big = sm.make_args(2**20, 2048)                                # batch x neg_tries = 2^31
+    big = sm.make_args(2**20, 2048, neg_tries=2048)               # batch x neg_tries = 2^31
     _expect(_call_sample(L, dag, big, ptrs), -6)
     _expect(_call_sample(L, dag, good, ptrs[:3] + [None] + ptrs[4:]), -1)   # negatives NULL
     a0 = sm.make_args(4, 0)
