@@ -227,6 +227,7 @@ def _workspace(ws, dag, args, stream=None):
 def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
                 workspace: "Workspace | None" = None) -> dict:
     """smore_sample into caller-owned torch tensors on the current (or given) stream."""
+    _require(out, _sample_shapes(args))
     wp, wn = _workspace(workspace, dag, args, stream)
     _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                               ctypes.byref(_out_struct(out)), wp, wn, _stream_handle(stream)))
@@ -247,6 +248,9 @@ def alloc_shared_outputs(batch: int, n_shared: int, device=None) -> dict:
 def sample_shared_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None,
                        workspace: "Workspace | None" = None) -> dict:
     """smore_sample_shared: args.n_neg is the size of the shared candidate set."""
+    b, n = args.batch, args.n_neg
+    _require(out, {"anchors": (b, 3), "relations": (b, 3), "positive": (b,), "pos_attempts": (b,),
+                   "shared": (n,), "n_shared": (1,), "mask": (b, (n + 31) // 32), "n_valid": (b,)})
     wp, wn = _workspace(workspace, dag, args, stream)
     st = SharedOut(*[out[k].data_ptr() if out[k].numel() else None for k in SHARED_FIELDS])
     _check(lib().smore_sample_shared(graph.handle, ctypes.byref(dag), ctypes.byref(args),
@@ -291,6 +295,41 @@ def verify(graph: Graph, qtype: "str | QueryDag", anchors, relations, candidates
     return out
 
 
+def _require(tensors: dict, shapes: dict, dtype_name: str = "int32") -> None:
+    """Caller-provided device buffers must have the sizes the kernels write:
+    the C ABI cannot see a device buffer's length."""
+    import torch
+    dtype = getattr(torch, dtype_name)
+    size = {}
+    for k, shape in shapes.items():
+        n = 1
+        for d in shape:
+            n *= d
+        size[k] = n
+        if tensors.get(k) is None and n:
+            raise ValueError(f"{k}: missing (needs {n} {dtype_name})")
+    dev = None
+    for k, shape in shapes.items():
+        t, n = tensors.get(k), size[k]
+        if t is None:
+            continue
+        if t.dtype != dtype or not t.is_cuda or not t.is_contiguous() or t.numel() != n:
+            raise ValueError(f"{k} must be a contiguous {dtype_name} device tensor of shape "
+                             f"{tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+        if dev is not None and t.device != dev:
+            raise ValueError(f"{k} is on {t.device}, other buffers on {dev}")
+        dev = t.device
+
+
+def _sample_shapes(args: SampleArgs, negatives: bool = True) -> dict:
+    b = args.batch
+    shapes = {"anchors": (b, 3), "relations": (b, 3), "positive": (b,), "n_valid": (b,),
+              "pos_attempts": (b,)}
+    if negatives:
+        shapes.update({"negatives": (b, args.n_neg), "neg_draws": (b,)})
+    return shapes
+
+
 def _out_struct(out: dict) -> SampleOut:
     return SampleOut(*[out[k].data_ptr() if k in out and out[k].numel() else None
                        for k in OUT_FIELDS])
@@ -306,6 +345,7 @@ def _stream_handle(stream):
 def sample_positives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream=None) -> dict:
     """First stage only (smore_sample_positives): anchors, relations, positive,
     pos_attempts, n_valid."""
+    _require(out, _sample_shapes(args, negatives=False))
     _check(lib().smore_sample_positives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                                         ctypes.byref(_out_struct(out)), _stream_handle(stream)))
     return out
@@ -317,6 +357,9 @@ def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, s
     stats: optional int64 [batch, 4] device tensor: (bytes, 64-byte lines) of
     graph data read per query by the candidate kernel, then by the kernel
     that intersects long lists."""
+    _require(out, _sample_shapes(args))
+    if stats is not None:
+        _require({"stats": stats}, {"stats": (args.batch, 4)}, "int64")
     sp = c_vp(stats.data_ptr()) if stats is not None else None
     wp, wn = _workspace(workspace, dag, args, stream)
     _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),

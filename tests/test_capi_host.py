@@ -45,6 +45,23 @@ def test_wait_hook_validation_on_host(L):
     assert L.smore_wait_before_kernel(None, 0) == 0
 
 
+def test_binding_rejects_wrong_output_buffers(L):
+    # the C ABI cannot see device buffer lengths, so the binding checks them
+    # before any call: here CPU tensors and a short negatives buffer
+    import torch
+    dag = sm.query_preset("2p")
+    args = sm.make_args(8, 4)
+    out = {k: torch.zeros(v, dtype=torch.int32) for k, v in
+           {"anchors": (8, 3), "relations": (8, 3), "positive": (8,), "negatives": (8, 4),
+            "n_valid": (8,), "pos_attempts": (8,), "neg_draws": (8,)}.items()}
+    with pytest.raises(ValueError, match="device tensor"):
+        sm.sample_into(None, dag, args, out)
+    with pytest.raises(ValueError):
+        sm.sample_negatives(None, dag, args, dict(out, negatives=torch.zeros((8, 3), dtype=torch.int32)))
+    with pytest.raises(ValueError, match="missing"):
+        sm.sample_positives(None, dag, args, {k: v for k, v in out.items() if k != "positive"})
+
+
 def test_exports_every_declared_function(L):
     names = declared_functions()
     assert len(names) >= 9
