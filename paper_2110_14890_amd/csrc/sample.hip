@@ -187,6 +187,13 @@ __device__ __forceinline__ bool has(const FSet& s, int32_t x, T&)
 // loops and exits that depend on it converged).
 __device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Lane k's copy of a value (k wave-uniform).
+__device__ __forceinline__ int32_t readlane(int32_t x, int k) { return __builtin_amdgcn_readlane(x, k); }
+__device__ __forceinline__ int64_t readlane64(int64_t x, int k)
+{
+    return (int64_t)(uint32_t)readlane((int32_t)x, k) | ((int64_t)readlane((int32_t)(x >> 32), k) << 32);
+}
+
 __device__ __forceinline__ uint64_t lanes_below(int lane)
 {
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
@@ -804,14 +811,11 @@ __device__ __forceinline__ int32_t deep_test(const GraphView& g, const FSet* F, 
 
 // Wavefront decision for a queued candidate (the one-hop operand of
 // pi / pin / pni has already been tested at lane level).
+// s is the candidate's backward list under the last relation (wave-uniform).
 template <int QT, class T>
-__device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel, int32_t c, int lane,
+__device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel, int2 s, int lane,
                            T& tl)
 {
-    const int32_t rb = chain_r1<QT> ? rel[1] : rel[2];
-    int2 s = group_range(g.rev, c, rb, tl);   // same address in every lane
-    s.x = uni(s.x);
-    s.y = uni(s.y);
     const int32_t* S = g.rev.nbr + s.x;
     const int32_t ns = s.y - s.x;
     if (QT == Q2P || QT == QPI || QT == QPIN) return wave_meet(S, ns, true, F[0].p, F[0].n, false, lane, tl);
@@ -1200,36 +1204,70 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
     }
 }
 
-// Persistent wavefronts draining the heavy queue.
+// Persistent wavefronts draining the heavy queue.  Wavefront w takes items
+// w, w + nwaves, ... (no shared counter to contend on).  It looks up its
+// next 64 items at once, one per lane: the queue entry, the candidate, the
+// query's relations and cached lists, and the candidate's backward list,
+// so those dependent reads overlap instead of preceding each test in turn.
 template <int QT, class T>
 __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p, smore_sample_out out,
                                                     Ws ws, int64_t* stats, int nxt)
 {
+    constexpr int NF = Shape<QT>::nf;
     const int lane = threadIdx.x & 63;
     // the compaction that follows appends to the next round's list
     if (blockIdx.x == 0 && threadIdx.x == 0) ws.ctrl[2 + nxt] = 0;
     const int32_t total = uni(ws.ctrl[0]);
     const int32_t nwaves = gridDim.x * (HEAVY_WG / 64);
+    const int32_t w0 = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6));
     T tl;
-    // wavefront w takes items w, w + nwaves, ... (no shared counter to contend on)
-    for (int32_t idx = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6)); idx < total;
-         idx += nwaves) {
-        const int2 it = ws.queue[idx];
-        const int32_t b = uni(it.x), j = uni(it.y);
-        const int64_t at = (int64_t)b * p.neg_tries + j;
-        const int32_t c = uni(ws.cval[at]);
-        int32_t rel[3];
-        for (int k = 0; k < 3; ++k) rel[k] = uni(out.relations[3 * (int64_t)b + k]);
-        const int32_t* qb = ws.qf + (int64_t)b * QF;
-        FSet F[3];
+    for (int64_t base = w0; base < total; base += 64 * (int64_t)nwaves) {
+        const int64_t mine = base + (int64_t)lane * nwaves;
+        int32_t mb = 0, mc = 0;
+        int64_t mat = 0;
+        int32_t mrel[3] = {0, 0, 0}, mf[2 * NF];
+        int2 ms = make_int2(0, 0);
 #pragma unroll
-        for (int f = 0; f < 3; ++f) {
-            const int32_t beg = uni(qb[2 * f]), end = uni(qb[2 * f + 1]);
-            F[f] = f < Shape<QT>::nf ? FSet{g.fwd.nbr + beg, end - beg, false} : FSet{nullptr, 0, true};
+        for (int f = 0; f < 2 * NF; ++f) mf[f] = 0;
+        if (mine < total) {
+            const int2 it = ws.queue[mine];
+            mb = it.x;
+            mat = (int64_t)it.x * p.neg_tries + it.y;
+            mc = ws.cval[mat];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) mrel[k] = out.relations[3 * (int64_t)mb + k];
+            const int32_t* qb = ws.qf + (int64_t)mb * QF;
+#pragma unroll
+            for (int f = 0; f < 2 * NF; ++f) mf[f] = qb[f];
+            ms = group_range(g.rev, mc, chain_r1<QT> ? mrel[1] : mrel[2]);
         }
-        const bool ans = heavy_test<QT>(g, F, rel, c, lane, tl);
-        if (lane == 0) ws.status[at] = ans ? ST_ANS : ST_NON;
-        flush_tally(tl, stats, b, lane, 2);
+        const int32_t n = uni((int32_t)min((int64_t)64, (total - base + nwaves - 1) / nwaves));
+        for (int k = 0; k < n; ++k) {
+            const int32_t b = readlane(mb, k);
+            int32_t rel[3];
+#pragma unroll
+            for (int q = 0; q < 3; ++q) rel[q] = readlane(mrel[q], k);
+            FSet F[3];
+#pragma unroll
+            for (int f = 0; f < 3; ++f) {
+                if (f < NF) {
+                    const int32_t beg = readlane(mf[2 * f], k), end = readlane(mf[2 * f + 1], k);
+                    F[f] = FSet{g.fwd.nbr + beg, end - beg, false};
+                } else {
+                    F[f] = FSet{nullptr, 0, true};
+                }
+            }
+            if constexpr (T::on) {
+                // the candidate's lookup, charged once to its query
+                T one;
+                (void)group_range(g.rev, readlane(mc, k), chain_r1<QT> ? rel[1] : rel[2], one);
+                if (lane == 0) tl = one;
+            }
+            const int2 s = make_int2(readlane(ms.x, k), readlane(ms.y, k));
+            const bool ans = heavy_test<QT>(g, F, rel, s, lane, tl);
+            if (lane == 0) ws.status[readlane64(mat, k)] = ans ? ST_ANS : ST_NON;
+            flush_tally(tl, stats, b, lane, 2);
+        }
     }
 }
 
