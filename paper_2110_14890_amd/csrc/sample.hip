@@ -567,7 +567,11 @@ template <> struct RootLists<Q2IN> { static constexpr int mask = 1, any = 0; };
 template <> struct RootLists<Q3IN> { static constexpr int mask = 3, any = 0; };
 template <> struct RootLists<QPNI> { static constexpr int mask = 2, any = 0; };
 
-constexpr int CWG = 256;         // threads of the candidate and compaction workgroups
+// The candidate kernel runs one wavefront per workgroup, and its first pass
+// one query per workgroup: queries differ widely in cost, and the hardware
+// dispatcher hands each freed slot the next query, where a fixed share per
+// wavefront leaves the kernel waiting on its slowest shares.
+constexpr int CWG = 64;
 constexpr int HEAVY_WG = 256;    // threads of the heavy-queue workgroups
 constexpr int QF = 8;            // int32 per query in the per-query block
 constexpr int PERSIST_BLOCKS = 2048;
@@ -1531,13 +1535,14 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         // later rounds carry the few queries short of n_neg: a smaller grid
         // keeps their (often empty) launches cheap
         const int grid = r == 0 ? PERSIST_BLOCKS : PERSIST_BLOCKS / 4;
+        const int cgrid = r == 0 ? max(p.batch, 1) : PERSIST_BLOCKS;   // one-wave workgroups
         if (r == 0 && g_wait) {
             const hipError_t e = hipStreamWaitEvent(st, g_wait, 0);
             g_wait = nullptr;
             if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
         }
         prof_mark(0, r, false, st);
-        k_candidates<QT, T><<<grid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
+        k_candidates<QT, T><<<cgrid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
         if ((rc = check_launch(err))) return rc;
         prof_mark(0, r, true, st);
         prof_mark(1, r, false, st);
@@ -1713,8 +1718,8 @@ int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out
     k_prepare<QT, NoTally><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, q, ws, nullptr, R);
     if ((rc = check_launch(err))) return rc;
     if (p.n_neg == 0) return SMORE_OK;
-    k_candidates<QT, NoTally, true><<<PERSIST_BLOCKS, CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
-                                                                    p.n_neg);
+    k_candidates<QT, NoTally, true><<<max(p.batch, 1), CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
+                                                                     p.n_neg);
     if ((rc = check_launch(err))) return rc;
     k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
     if ((rc = check_launch(err))) return rc;
