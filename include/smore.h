@@ -122,7 +122,10 @@ int smore_graph_info(const smore_graph *g, int64_t *n_entities, int64_t *n_relat
    4 rev groups, 5 rev neighbours, 6 active_in (entities with an in-edge,
    ascending), 7 in-edge mask [(V+31)/32] (bit v % 32 of word v / 32 set
    iff entity v has an in-edge), 8 coarse in-edge mask [(V+127)/128] (bit
-   i % 32 of word i / 32 set iff one of entities 4i .. 4i+3 has an in-edge).
+   i % 32 of word i / 32 set iff one of entities 4i .. 4i+3 has an in-edge),
+   9 in-relation signatures [(V+3)/4] (byte v % 4 of word v / 4, little
+   endian, is entity v's: bit (r * 0x9E3779B1 mod 2^32) >> 29 set for each
+   relation r of its in-edges, 0 for an entity without in-edges).
    count must equal the array length.
    Synchronous. */
 int smore_graph_copy(const smore_graph *g, int32_t which, int32_t *host_dst, int64_t count);

@@ -367,6 +367,7 @@ int smore_graph_copy(const smore_graph* g, int32_t which, int32_t* host_dst, int
         case 6: src = g->active_in; n = g->n_active; break;
         case 7: src = g->has_in; n = ((int64_t)g->V + 31) / 32; break;
         case 8: src = g->has_in4; n = ((int64_t)g->V + 127) / 128; break;
+        case 9: src = g->sig; n = ((int64_t)g->V + 3) / 4; break;
         default: return fail(SMORE_E_INVALID_ARG, "unknown array %d", which);
     }
     if (count != n) return fail(SMORE_E_INVALID_ARG, "array %d has %lld entries, not %lld", which,
@@ -412,7 +413,7 @@ void smore_free_graph(smore_graph* g)
     (void)hipGetDevice(&cur);
     if (cur != g->device) (void)hipSetDevice(g->device);
     void* bufs[] = {g->f_node, g->f_grp, g->f_nbr, g->r_node, g->r_grp, g->r_nbr, g->active_in,
-                    g->has_in, g->has_in4};
+                    g->has_in, g->has_in4, g->sig};
     for (void* b : bufs)
         if (b) (void)hipFree(b);
     if (cur >= 0 && cur != g->device) (void)hipSetDevice(cur);

@@ -267,6 +267,24 @@ __global__ void k_has_in4(const uint32_t* __restrict__ bits, int64_t words, uint
     coarse[w] = out;
 }
 
+// in-relation signatures of entities 4w .. 4w + 3, one byte each: the OR
+// of sig_bit(r) over the relations r of the entity's reverse groups
+__global__ void k_sig(const int32_t* __restrict__ node, const int2* __restrict__ grp, int32_t V,
+                      uint32_t* __restrict__ out)
+{
+    const int64_t w = (int64_t)blockIdx.x * BT + threadIdx.x;
+    if (w * 4 >= V) return;
+    uint32_t word = 0;
+    for (int b = 0; b < 4; ++b) {
+        const int64_t v = w * 4 + b;
+        if (v >= V) break;
+        uint32_t sg = 0;
+        for (int32_t k = node[v]; k < node[v + 1]; ++k) sg |= sig_bit(grp[k].x);
+        word |= sg << (8 * b);
+    }
+    out[w] = word;
+}
+
 inline unsigned grid_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // Owns temporary device buffers for the duration of a build.
@@ -514,9 +532,13 @@ int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_
     TRY(hipMalloc(&g->has_in4, (size_t)cwords * 4));
     k_has_in4<<<grid_for(cwords, BT), BT>>>(g->has_in, words, g->has_in4);
     TRY(hipGetLastError());
+    const int64_t swords = ((int64_t)V + 3) / 4;
+    TRY(hipMalloc(&g->sig, (size_t)(swords > 0 ? swords : 1) * 4));
+    k_sig<<<grid_for(swords, BT), BT>>>(g->r_node, g->r_grp, V, (uint32_t*)g->sig);
+    TRY(hipGetLastError());
     TRY(hipDeviceSynchronize());
     g->n_active = na;
-    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na + words + cwords) * 4 +
+    g->bytes = (size_t)(2 * ((int64_t)V + 1) + 2 * E + na + words + cwords + swords) * 4 +
                (size_t)(g->S_fwd + g->S_rev + 2) * sizeof(int2);
     return SMORE_OK;
 }

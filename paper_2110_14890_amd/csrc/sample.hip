@@ -556,6 +556,25 @@ template <int QT> constexpr bool two_cached = QT == QIP || QT == QUP || QT == QI
 // only if c is in list f for every f of `mask` (any f when `any`).  When
 // these lists are staged in LDS they decide the draws without a single
 // graph read; otherwise the in-edge mask does.
+// Relation slots of the projections that end at the root (bit s: slot s),
+// positive operands only: an answer has an in-edge under each of them (any
+// one of them for a union).
+template <int QT> struct RootRels { static constexpr int mask = 0, any = 0; };
+template <> struct RootRels<Q1P> { static constexpr int mask = 1, any = 0; };
+template <> struct RootRels<Q2P> { static constexpr int mask = 2, any = 0; };
+template <> struct RootRels<Q3P> { static constexpr int mask = 4, any = 0; };
+template <> struct RootRels<Q2I> { static constexpr int mask = 3, any = 0; };
+template <> struct RootRels<Q3I> { static constexpr int mask = 7, any = 0; };
+template <> struct RootRels<QIP> { static constexpr int mask = 4, any = 0; };
+template <> struct RootRels<QPI> { static constexpr int mask = 6, any = 0; };
+template <> struct RootRels<Q2U> { static constexpr int mask = 3, any = 1; };
+template <> struct RootRels<QUP> { static constexpr int mask = 4, any = 0; };
+template <> struct RootRels<Q2IN> { static constexpr int mask = 1, any = 0; };
+template <> struct RootRels<Q3IN> { static constexpr int mask = 3, any = 0; };
+template <> struct RootRels<QINP> { static constexpr int mask = 4, any = 0; };
+template <> struct RootRels<QPIN> { static constexpr int mask = 2, any = 0; };
+template <> struct RootRels<QPNI> { static constexpr int mask = 4, any = 0; };
+
 template <int QT> struct RootLists { static constexpr int mask = 0, any = 0; };
 template <> struct RootLists<Q1P> { static constexpr int mask = 1, any = 0; };
 template <> struct RootLists<Q2I> { static constexpr int mask = 3, any = 0; };
@@ -1070,6 +1089,11 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
         // are in flight
         constexpr int RM = RootLists<QT>::mask;
         const bool use_lists = RM != 0 && (RootLists<QT>::any ? (staged & RM) == RM : (staged & RM) != 0);
+        // signature bits an answer must carry
+        uint32_t need = 0;
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            if (RootRels<QT>::mask >> k & 1) need |= sig_bit(rel[k]);
         bool to_stage = used > 0;
         if (use_lists) {
             stage_lists();
@@ -1081,7 +1105,10 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             // bits, resident in the last-level cache) decides most draws.
             // On a large graph the coarse mask (one bit per four entities,
             // small enough for the L2) is read first, and only draws whose
-            // group of four has an in-edge read the fine mask.
+            // group of four has an in-edge read their in-relation
+            // signature (a byte per entity), which must hold the bits of
+            // the relations that end at the root: a draw with in-edges
+            // only under other relation classes is a non-answer too.
             int32_t c[DPW];
             uint32_t word[DPW];
             const bool two_level = !use_lists && g.coarse;
@@ -1113,7 +1140,9 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                     const bool live = base + k * 64 + lane < j1 && c[k] >= 0;
                     const bool maybe = live && ((word[k] >> ((c[k] >> 2) & 31)) & 1u);
                     if (live) tl.read(g.has_in4 + (c[k] >> 7), 4);
-                    word[k] = maybe ? g.has_in[c[k] >> 5] : 0u;
+                    const uint32_t sg = maybe ? (uint32_t)g.sig[c[k]] : 0u;
+                    const bool pass = RootRels<QT>::any ? (sg & need) != 0 : (sg & need) == need;
+                    word[k] = pass ? ~0u : 0u;
                 }
             }
             if (use_lists) {
@@ -1758,6 +1787,7 @@ GraphView view_of(const smore_graph* g)
     gv.active_in = g->active_in;
     gv.has_in = g->has_in;
     gv.has_in4 = g->has_in4;
+    gv.sig = g->sig;
     // above 2 MiB of fine mask (V > 2^24) the coarse mask (a quarter of
     // the size) answers most draws from the L2
     gv.coarse = g->V > (1 << 24);

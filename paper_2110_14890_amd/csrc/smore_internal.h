@@ -25,7 +25,9 @@ struct GraphView {
     const int32_t* active_in;  // entities with an in-edge, ascending
     const uint32_t* has_in;    // bit v: entity v has an in-edge (V bits, cache-resident)
     const uint32_t* has_in4;   // bit i: one of entities 4i .. 4i + 3 has an in-edge (V / 4 bits)
-    int32_t coarse;            // test has_in4 before has_in (when has_in outgrows the L2)
+    const uint8_t* sig;        // in-relation signature of entity v: bit sig_bit(r) set for
+                               // each relation r of its in-edges (V bytes, 0 without in-edge)
+    int32_t coarse;            // test has_in4, then sig (when has_in outgrows the L2)
     int32_t V;
     int32_t n_active;
 };
@@ -81,6 +83,13 @@ struct SampleParams {
 
 }  // namespace smore
 
+// Bit of relation r in an entity's in-relation signature (eight classes,
+// multiplicative hash of the relation id).
+__host__ __device__ inline uint32_t sig_bit(int32_t r)
+{
+    return 1u << (((uint32_t)r * 0x9E3779B1u) >> 29);
+}
+
 struct smore_graph {
     int device;
     int32_t V, R;
@@ -88,6 +97,7 @@ struct smore_graph {
     int32_t *f_node, *f_nbr, *r_node, *r_nbr, *active_in;
     int2 *f_grp, *r_grp;
     uint32_t *has_in, *has_in4;
+    uint8_t* sig;
     size_t bytes;
 };
 

@@ -48,6 +48,14 @@ def check_graph(g, og):
     cw = g.copy(8, (g.V + 127) // 128).view(np.uint32)
     cbits = np.unpackbits(cw.view(np.uint8), bitorder="little")
     assert np.array_equal(np.nonzero(cbits)[0], np.unique(og.active_in() // 4))
+    # in-relation signatures: byte v is the OR over v's in-edges (t = v,
+    # relation r) of bit (r * 0x9E3779B1 mod 2^32) >> 29
+    sig = g.copy(9, (g.V + 3) // 4).view(np.uint8)[:g.V]
+    te, tr_rel, _ = og.dump(reverse=True)
+    want = np.zeros(g.V, np.uint8)
+    cls = ((tr_rel.astype(np.uint64) * 0x9E3779B1) & 0xFFFFFFFF) >> 29
+    np.bitwise_or.at(want, te, (1 << cls).astype(np.uint8))
+    assert np.array_equal(sig, want)
 
 
 @pytest.mark.parametrize("case", ["dups", "dups_inverse", "tiny", "fb15k237", "fb400k", "empty",
@@ -140,23 +148,29 @@ def test_graph_without_in_edges_of_depth():
     assert (got["n_valid"] == -1).all()
 
 
+@pytest.mark.parametrize("R", [8, 300])
 @pytest.mark.parametrize("qt", sm.TYPES)
-def test_two_level_in_edge_mask(qt):
+def test_two_level_in_edge_mask(qt, R):
     # more than 2^24 entities: the candidate kernel tests the coarse mask
-    # (one bit per four entities) before the fine one; 100,000 entities
-    # scattered over 20,000,000 ids hold every edge
+    # (one bit per four entities), then the in-relation signature; 100,000
+    # entities scattered over 20,000,000 ids hold every edge (with 300
+    # relations most entities miss most signature classes)
     rng = np.random.default_rng(17)
     V = 20_000_000
     ents = rng.choice(V, 100_000, replace=False).astype(np.int32)
-    tr = np.stack([ents[rng.integers(0, len(ents), 400_000)], rng.integers(0, 8, 400_000),
+    tr = np.stack([ents[rng.integers(0, len(ents), 400_000)], rng.integers(0, R, 400_000),
                    ents[rng.integers(0, len(ents), 400_000)]], axis=1).astype(np.int32)
-    g, og = graph_pair(tr, V, 8)
+    g, og = graph_pair(tr, V, R)
+    if R == 300:
+        check_graph(g, og)
     for n_neg, nt in [(64, 256), (600, 2400)]:
-        progress(f"two-level mask {qt} n_neg {n_neg}")
+        progress(f"two-level mask {qt} R {R} n_neg {n_neg}")
         got = gpu_sample(g, qt, 512, n_neg, seed=5, neg_tries=nt)
         ref = og.sample(qt, 512, n_neg, seed=5, neg_tries=nt)
         assert_same(got, ref, what=f"{qt} n_neg {n_neg}")
-        assert (got["n_valid"] >= 0).mean() > 0.5
+        # enough valid queries to exercise the path (fewer shapes ground
+        # a positive on the sparser 300-relation graph: 17% for 3in)
+        assert (got["n_valid"] >= 0).mean() > (0.5 if R == 8 else 0.1)
 
 
 def test_single_entity_graph_and_single_query():
