@@ -1006,8 +1006,9 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     }
 }
 
-// One wavefront per active query (persistent over the list, several
-// queries per workgroup and no workgroup barrier).  The query's lists are
+// One wavefront per active query, in one-wave workgroups: a workgroup per
+// query in the first round, persistent over the list in later rounds (no
+// workgroup barrier).  The query's lists are
 // staged once into the wave's LDS slice.  Draws are taken WIN at a time:
 // every lane computes WIN / 64 draws and reads their in-edge bits (all
 // loads in flight together); the draws with an in-edge are compacted into
