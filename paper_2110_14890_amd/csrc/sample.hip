@@ -803,19 +803,27 @@ __device__ __forceinline__ int32_t deep_test(const GraphView& g, const FSet* F, 
         // pni: a meeting chain means c is in the complemented set
         return (QT == QPNI ? !hit : hit) ? ST_ANS : ST_NON;
     }
-    // 3p: node pairs of every y at once, then each y's group under r1
+    // 3p: node pairs and signatures of every y at once, then each y's
+    // group under r1 (skipped when y's signature lacks r1's class: y then
+    // has no in-edge under r1)
     int32_t a0[LANE_SEG], a1[LANE_SEG];
+    uint32_t sg[LANE_SEG];
+    const uint32_t b1 = sig_bit(rel[1]);
 #pragma unroll
     for (int k = 0; k < LANE_SEG; ++k) {
         a0[k] = 0;
         a1[k] = 0;
+        sg[k] = 0;
         if (k < len) {
             a0[k] = g.rev.node[y[k]];
             a1[k] = g.rev.node[y[k] + 1];
+            sg[k] = g.sig[y[k]];
             tl.read(g.rev.node + y[k], 8);
+            tl.read(g.sig + y[k], 1);
         }
     }
     for (int k = 0; k < len; ++k) {
+        if (!(sg[k] & b1)) continue;
         const int2 s2 = group_find(g.rev, a0[k], a1[k], rel[1], tl);
         const int32_t n2 = s2.y - s2.x;
         if (n2 > LANE_SEG) return ST_PEND;
@@ -856,7 +864,12 @@ __device__ bool heavy_test(const GraphView& g, const FSet* F, const int32_t* rel
         for (int32_t k = 0; k < ns; k += 64) {
             if (lane == 0) tl.read(S + k, 4 * min(64, ns - k));
             int2 s2 = make_int2(0, 0);
-            if (k + lane < ns) s2 = group_range(g.rev, S[k + lane], rel[1], tl);
+            if (k + lane < ns) {
+                // y without an in-edge under r1's signature class has none under r1
+                const int32_t y = S[k + lane];
+                tl.read(g.sig + y, 1);
+                if (g.sig[y] & sig_bit(rel[1])) s2 = group_range(g.rev, y, rel[1], tl);
+            }
             const int32_t len = s2.y - s2.x;
             const bool keys_in_list = len <= F[0].n;       // search R_r1(y) entries in F0
             const int32_t npair = len > 0 ? min(len, F[0].n) : 0;
