@@ -301,6 +301,9 @@ def main():
                     help="run the shapes of a step one after another on one stream "
                          "(default: one stream per shape; a shape's negatives start when the "
                          "previous shape's candidate kernel ends)")
+    ap.add_argument("--split", action="store_true",
+                    help="candidate kernels of all shapes back to back on one stream "
+                         "(smore_sample_negatives_part); the rest on each shape's stream")
     ap.add_argument("--prepare-ahead", action="store_true",
                     help="with one stream per shape, let a shape's preparation run before the "
                          "wait for the previous candidate kernel (smore_wait_before_kernel)")
@@ -390,25 +393,60 @@ def main():
     # while positives and the long-list and selection kernels of other
     # shapes run beside it.
     # The streams join the timing stream only at the ends of the timed region.
+    # With --split the chain needs no cross-stream waits: every shape's
+    # first-round candidate kernel runs on one candidate stream, in chain
+    # order, after its preparation on the shape's stream (an event), and the
+    # shape's stream takes up the rest of its negatives after it (an event).
     streams = {qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
+    cand_stream = torch.cuda.Stream() if args.split else None
+    all_streams = list(streams.values()) + ([cand_stream] if cand_stream is not None else [])
     join = {qt: torch.cuda.Event() for qt in types}
     chain = [None]   # end event of the last candidate kernel launched
+    parts_ws = {qt: sm.Workspace() for qt in types}
+    prepared = {qt: torch.cuda.Event() for qt in types}
+    drawn = {qt: torch.cuda.Event() for qt in types}
 
     def fork():
         join["fork"] = torch.cuda.Event()
         join["fork"].record(stream)
-        for qt in types:
-            if streams[qt] is not stream:
-                streams[qt].wait_event(join["fork"])
+        for s in all_streams:
+            if s is not stream:
+                s.wait_event(join["fork"])
 
     def merge():
-        for qt in types:
-            if streams[qt] is not stream:
-                join[qt].record(streams[qt])
-                stream.wait_event(join[qt])
+        for i, s in enumerate(all_streams):
+            if s is not stream:
+                e = join.setdefault(i, torch.cuda.Event())
+                e.record(s)
+                stream.wait_event(e)
         chain[0] = None
 
+    def split_step(ev):
+        for qt in types:
+            s = streams[qt]
+            ev[qt][0].record(s)
+            sm.sample_positives(g, dags[qt], argv[qt], outs[qt], s)
+            ev[qt][1].record(s)
+            ev[qt][5].record(s)
+            sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s, part=sm.NEG_PREPARE,
+                                workspace=parts_ws[qt])
+            prepared[qt].record(s)
+        for qt in types:
+            s = streams[qt]
+            cand_stream.wait_event(prepared[qt])
+            sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
+            sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, cand_stream,
+                                part=sm.NEG_CANDIDATES, workspace=parts_ws[qt])
+            drawn[qt].record(cand_stream)
+            s.wait_event(drawn[qt])
+            sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s, part=sm.NEG_REST,
+                                workspace=parts_ws[qt])
+            ev[qt][2].record(s)
+
     def step(ev):
+        if args.split:
+            split_step(ev)
+            return
         for qt in types:   # positives first: they wait for nothing but their own stream
             s = streams[qt]
             ev[qt][0].record(s)
@@ -455,6 +493,18 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
     log(f"host enqueue {host_ms:.3f} ms per step, device {ms_step:.3f} ms per step")
+    # the schedule must not change a row: the last timed step's outputs
+    # against one plain call per shape on the timing stream
+    for qt in types:
+        ref = sm.alloc_outputs(cfg.batch, cfg.n_neg)
+        sm.sample_positives(g, dags[qt], argv[qt], ref, stream)
+        sm.sample_negatives(g, dags[qt], argv[qt], ref, None, stream)
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            if not torch.equal(v, outs[qt][k]):
+                raise SystemExit(f"bench: {qt} {k} of the timed schedule differs from a plain call")
+        del ref
+    log("schedule check: every shape's rows equal those of a plain call")
     per_type = {}
     for qt in types:
         pos = float(np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs]))
@@ -463,7 +513,7 @@ def main():
         a = acct[qt]
         # with --prepare-ahead the negative stage includes the wait for the
         # previous shape's candidate kernel: no per-shape rates then
-        rated = not args.prepare_ahead
+        rated = not (args.prepare_ahead or args.split)
         per_type[qt] = {
             "queries_per_s": cfg.batch / ((pos + neg) / 1e3) if rated else None,
             "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3) if rated else None,
@@ -494,6 +544,10 @@ def main():
                 "avg_launch_ms": round(d["candidate_kernel_ms"], 4),
                 "launch_timing": ("HIP events around the launch on its stream, one stream for the step"
                                   if args.serial else
+                                  "HIP events around the launch on the candidate stream, where the "
+                                  "shapes' candidate kernels run back to back; positives and the "
+                                  "long-list and selection kernels run beside it on the shapes' streams"
+                                  if args.split else
                                   "HIP events around the launch on its shape's stream; positives and the "
                                   "long-list and selection kernels of other shapes may run beside it"),
                 "accounting": "64-byte lines of graph data per dependent read of the candidate "
@@ -517,7 +571,9 @@ def main():
         "config": {"workload": workload_name(cfg, types), "types": types, "batch": cfg.batch,
                    "n_neg": cfg.n_neg, "neg_tries": neg_tries, "pos_tries": 64,
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed,
-                   "streams": 1 if args.serial else len(types)},
+                   "streams": 1 if args.serial else len(types) + (1 if args.split else 0),
+                   "schedule": "serial" if args.serial else "split" if args.split else
+                               "chained, prepare ahead" if args.prepare_ahead else "chained"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "gather_ceiling": ceiling,

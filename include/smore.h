@@ -203,6 +203,26 @@ int smore_sample_negatives(const smore_graph *g, const smore_query_dag *dag,
                            const smore_sample_args *args, const smore_sample_out *out,
                            int64_t *stats, void *workspace, size_t ws_bytes, void *hip_stream);
 
+/* smore_sample_negatives in three parts, for callers that schedule the
+   first round's candidate kernel (the verification of the first batch of
+   rejection-sampling draws, Sec. 3.2) apart from the rest, e.g. the
+   candidate kernels of several calls back to back on one stream:
+   part 0 the per-query preparation, part 1 the first round's candidate
+   kernel, part 2 the rest (long lists, ordered selection, later rounds).
+   Calling parts 0, 1 and 2 with the same arguments, outputs and workspace,
+   each after the previous one has completed in stream order (on one stream,
+   or ordered by the caller's events across streams), has exactly the effect
+   of one smore_sample_negatives call; the outputs are final only after
+   part 2.  The workspace carries state from part to part: it must not be
+   used by any other call in between.  stats, the instrumentation hooks and
+   errors as for smore_sample_negatives (smore_profile_kernel's candidate
+   kernel and smore_wait_before_kernel act in part 1; any part disarms
+   them).  SMORE_E_INVALID_ARG for another part. */
+int smore_sample_negatives_part(const smore_graph *g, const smore_query_dag *dag,
+                                const smore_sample_args *args, const smore_sample_out *out,
+                                int64_t *stats, int32_t part, void *workspace, size_t ws_bytes,
+                                void *hip_stream);
+
 /* Caller-owned device outputs of smore_sample_shared, int32 unless noted.
    anchors [B,3], relations [B,3], positive [B], pos_attempts [B]
                      as in smore_sample_out

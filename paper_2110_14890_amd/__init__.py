@@ -95,6 +95,10 @@ def lib() -> ctypes.CDLL:
         L.smore_sample_negatives.argtypes = [c_vp, ctypes.POINTER(QueryDag),
                                              ctypes.POINTER(SampleArgs), ctypes.POINTER(SampleOut),
                                              c_vp, c_vp, ctypes.c_size_t, c_vp]
+        L.smore_sample_negatives_part.argtypes = [c_vp, ctypes.POINTER(QueryDag),
+                                                  ctypes.POINTER(SampleArgs),
+                                                  ctypes.POINTER(SampleOut), c_vp, c_i32, c_vp,
+                                                  ctypes.c_size_t, c_vp]
         L.smore_profile_kernel.argtypes = [c_vp, c_vp, c_i32]
         L.smore_wait_before_kernel.argtypes = [c_vp, c_i32]
         L.smore_gather_probe.argtypes = [c_vp, c_i64, c_i64, c_vp, c_i64, c_vp]
@@ -351,20 +355,32 @@ def sample_positives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, s
     return out
 
 
+NEG_PREPARE, NEG_CANDIDATES, NEG_REST = 0, 1, 2
+
+
 def sample_negatives(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stats=None,
-                     stream=None, workspace: "Workspace | None" = None) -> dict:
+                     stream=None, workspace: "Workspace | None" = None, part=None) -> dict:
     """Second stage only (smore_sample_negatives) on the queries in `out`;
     stats: optional int64 [batch, 4] device tensor: (bytes, 64-byte lines) of
     graph data read per query by the candidate kernel, then by the kernel
-    that intersects long lists."""
+    that intersects long lists.  part: None for the whole stage, else one of
+    NEG_PREPARE, NEG_CANDIDATES, NEG_REST (smore_sample_negatives_part: the
+    caller orders the three parts and passes the same workspace to each)."""
+    if part is not None and workspace is None:
+        raise ValueError("the parts of one negatives call must share an explicit workspace")
     _require(out, _sample_shapes(args))
     if stats is not None:
         _require({"stats": stats}, {"stats": (args.batch, 4)}, "int64")
     sp = c_vp(stats.data_ptr()) if stats is not None else None
     wp, wn = _workspace(workspace, dag, args, stream)
-    _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
-                                        ctypes.byref(_out_struct(out)), sp, wp, wn,
-                                        _stream_handle(stream)))
+    if part is None:
+        _check(lib().smore_sample_negatives(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                            ctypes.byref(_out_struct(out)), sp, wp, wn,
+                                            _stream_handle(stream)))
+    else:
+        _check(lib().smore_sample_negatives_part(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                                 ctypes.byref(_out_struct(out)), sp, part, wp, wn,
+                                                 _stream_handle(stream)))
     return out
 
 

@@ -506,7 +506,7 @@ smore::SampleParams params_of(const smore_sample_args* a)
 // Validation shared by the sampling entry points, then the launch(es).
 int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
                const smore_sample_out* out, int64_t* stats, void* workspace, size_t ws_bytes,
-               void* hip_stream, int stages)
+               void* hip_stream, int stages, int parts = smore::NEG_ALL)
 {
     // host-side checks first (they need no device), the graph last
     if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
@@ -531,7 +531,7 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
         if (a->n_neg > 0 && (!workspace || ws_bytes < smore::negatives_workspace_bytes(p)))
             return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
                         smore::negatives_workspace_bytes(p));
-        rc = smore::launch_negative(g, (smore::QType)qt, p, *out, stats, workspace, ws_bytes,
+        rc = smore::launch_negative(g, (smore::QType)qt, p, *out, stats, workspace, ws_bytes, parts,
                                     (hipStream_t)hip_stream, &err);
         if (rc) return fail(rc, "negative sampling: %s", err);
     }
@@ -617,6 +617,15 @@ int smore_sample_negatives(const smore_graph* g, const smore_query_dag* dag,
                            void* workspace, size_t ws_bytes, void* hip_stream)
 {
     return run_sample(g, dag, a, out, stats, workspace, ws_bytes, hip_stream, NEG);
+}
+
+int smore_sample_negatives_part(const smore_graph* g, const smore_query_dag* dag,
+                                const smore_sample_args* a, const smore_sample_out* out,
+                                int64_t* stats, int32_t part, void* workspace, size_t ws_bytes,
+                                void* hip_stream)
+{
+    if (part < 0 || part > 2) return fail(SMORE_E_INVALID_ARG, "part must be 0, 1 or 2");
+    return run_sample(g, dag, a, out, stats, workspace, ws_bytes, hip_stream, NEG, 1 << part);
 }
 
 }  // extern "C"

@@ -1562,32 +1562,40 @@ inline void prof_mark(int which, int round, bool after, hipStream_t st)
     if (after) g_prof = ProfileArm{};
 }
 
+// parts: NEG_PREPARE the per-query preparation, NEG_CANDIDATES the first
+// round's candidate kernel, NEG_REST the first round's long-list and
+// selection kernels and every later round.
 template <int QT, class T>
 int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample_out& out, Ws ws,
-                  int64_t* stats, int32_t R, hipStream_t st, const char** err)
+                  int64_t* stats, int32_t R, int parts, hipStream_t st, const char** err)
 {
     int rc;
-    k_prepare<QT, T><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, out, ws, stats, R);
-    if ((rc = check_launch(err))) return rc;
+    if (parts & NEG_PREPARE) {
+        k_prepare<QT, T><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, out, ws, stats, R);
+        if ((rc = check_launch(err))) return rc;
+    }
     if (p.n_neg == 0) return SMORE_OK;
     const int rounds = n_rounds(p);
-    int32_t prev = 0;
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
+        const int32_t prev = r == 0 ? 0 : round_end(p, r - 1);   // the round's first draw
         const int32_t j_end = round_end(p, r);
         // later rounds carry the few queries short of n_neg: a smaller grid
         // keeps their (often empty) launches cheap
         const int grid = r == 0 ? PERSIST_BLOCKS : PERSIST_BLOCKS / 4;
         const int cgrid = r == 0 ? max(p.batch, 1) : PERSIST_BLOCKS;   // one-wave workgroups
-        if (r == 0 && g_wait) {
-            const hipError_t e = hipStreamWaitEvent(st, g_wait, 0);
-            g_wait = nullptr;
-            if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
+        if (parts & (r == 0 ? NEG_CANDIDATES : NEG_REST)) {
+            if (r == 0 && g_wait) {
+                const hipError_t e = hipStreamWaitEvent(st, g_wait, 0);
+                g_wait = nullptr;
+                if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
+            }
+            prof_mark(0, r, false, st);
+            k_candidates<QT, T><<<cgrid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
+            if ((rc = check_launch(err))) return rc;
+            prof_mark(0, r, true, st);
         }
-        prof_mark(0, r, false, st);
-        k_candidates<QT, T><<<cgrid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
-        if ((rc = check_launch(err))) return rc;
-        prof_mark(0, r, true, st);
+        if (!(parts & NEG_REST)) continue;
         prof_mark(1, r, false, st);
         k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
@@ -1607,7 +1615,6 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                                                                   r == rounds - 1, tcap, tshift, r == 0);
             if ((rc = check_launch(err))) return rc;
             prof_mark(2, r, true, st);
-            prev = j_end;
             continue;
         }
         const int32_t tcap = compact_tcap(j_end);
@@ -1627,30 +1634,29 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                                                        tshift);
         if ((rc = check_launch(err))) return rc;
         prof_mark(2, r, true, st);
-        prev = j_end;
     }
     return SMORE_OK;
 }
 
 template <class T>
 int dispatch_negatives(QType qt, const GraphView& gv, const SampleParams& p, const smore_sample_out& out,
-                       Ws ws, int64_t* stats, int32_t R, hipStream_t st, const char** err)
+                       Ws ws, int64_t* stats, int32_t R, int parts, hipStream_t st, const char** err)
 {
     switch (qt) {
-        case Q1P: return run_negatives<Q1P, T>(gv, p, out, ws, stats, R, st, err);
-        case Q2P: return run_negatives<Q2P, T>(gv, p, out, ws, stats, R, st, err);
-        case Q3P: return run_negatives<Q3P, T>(gv, p, out, ws, stats, R, st, err);
-        case Q2I: return run_negatives<Q2I, T>(gv, p, out, ws, stats, R, st, err);
-        case Q3I: return run_negatives<Q3I, T>(gv, p, out, ws, stats, R, st, err);
-        case QIP: return run_negatives<QIP, T>(gv, p, out, ws, stats, R, st, err);
-        case QPI: return run_negatives<QPI, T>(gv, p, out, ws, stats, R, st, err);
-        case Q2U: return run_negatives<Q2U, T>(gv, p, out, ws, stats, R, st, err);
-        case QUP: return run_negatives<QUP, T>(gv, p, out, ws, stats, R, st, err);
-        case Q2IN: return run_negatives<Q2IN, T>(gv, p, out, ws, stats, R, st, err);
-        case Q3IN: return run_negatives<Q3IN, T>(gv, p, out, ws, stats, R, st, err);
-        case QINP: return run_negatives<QINP, T>(gv, p, out, ws, stats, R, st, err);
-        case QPIN: return run_negatives<QPIN, T>(gv, p, out, ws, stats, R, st, err);
-        case QPNI: return run_negatives<QPNI, T>(gv, p, out, ws, stats, R, st, err);
+        case Q1P: return run_negatives<Q1P, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q2P: return run_negatives<Q2P, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q3P: return run_negatives<Q3P, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q2I: return run_negatives<Q2I, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q3I: return run_negatives<Q3I, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QIP: return run_negatives<QIP, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QPI: return run_negatives<QPI, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q2U: return run_negatives<Q2U, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QUP: return run_negatives<QUP, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q2IN: return run_negatives<Q2IN, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case Q3IN: return run_negatives<Q3IN, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QINP: return run_negatives<QINP, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QPIN: return run_negatives<QPIN, T>(gv, p, out, ws, stats, R, parts, st, err);
+        case QPNI: return run_negatives<QPNI, T>(gv, p, out, ws, stats, R, parts, st, err);
         default: *err = "unknown shape"; return SMORE_E_UNSUPPORTED;
     }
 }
@@ -1839,7 +1845,7 @@ int launch_positive(const smore_graph* g, const WalkProgram& wp, const SamplePar
 
 int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
                     const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
-                    hipStream_t st, const char** err)
+                    int parts, hipStream_t st, const char** err)
 {
     Ws ws;
     const size_t need = ws_layout(p, &ws, (char*)workspace);
@@ -1848,8 +1854,8 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
         return SMORE_E_INVALID_ARG;
     }
     const GraphView gv = view_of(g);
-    const int rc = stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, st, err)
-                         : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, st, err);
+    const int rc = stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, parts, st, err)
+                         : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, parts, st, err);
     g_prof = ProfileArm{};  // one-shot: an arm never outlives the call it was meant for
     g_wait = nullptr;
     return rc;

@@ -107,9 +107,11 @@ int build_graph_device(const int32_t* triples_host, int64_t n, int32_t V, int32_
                        bool add_inverse, smore_graph* g, const char** err);
 int launch_positive(const smore_graph* g, const WalkProgram& wp, const SampleParams& p,
                     const smore_sample_out& out, hipStream_t stream, const char** err);
+// Parts of the negative stage (bit masks for launch_negative).
+constexpr int NEG_PREPARE = 1, NEG_CANDIDATES = 2, NEG_REST = 4, NEG_ALL = 7;
 int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
                     const smore_sample_out& out, int64_t* stats, void* workspace, size_t ws_bytes,
-                    hipStream_t stream, const char** err);
+                    int parts, hipStream_t stream, const char** err);
 size_t negatives_workspace_bytes(const SampleParams& p);
 int launch_shared(const smore_graph* g, QType qt, const SampleParams& p, const smore_sample_out& pos,
                   int32_t* shared, int32_t* n_shared, uint32_t* mask, void* workspace,

@@ -230,6 +230,38 @@ def test_sample_validation_on_host(L):
     _expect(_call_sample(L, other, good, ptrs), -3)
 
 
+def test_negatives_part_validation_on_host(L):
+    # the part number is checked first, then the same checks as
+    # smore_sample_negatives (the graph last); the binding requires the
+    # parts of one call to share an explicit workspace
+    buf = (ctypes.c_int32 * 64)()
+    so = sm.SampleOut(*([ctypes.addressof(buf)] * 7))
+    dag = sm.query_preset("3p")
+    a = sm.make_args(4, 2)
+
+    def call(part, args=a):
+        return L.smore_sample_negatives_part(None, ctypes.byref(dag), ctypes.byref(args),
+                                             ctypes.byref(so), None, part, None, 0, None)
+    for part in (-1, 3):
+        _expect(call(part), -1)
+        assert "part" in sm.last_error()
+    for part in (0, 1, 2):
+        _expect(call(part), -1)
+        assert "graph" in sm.last_error()
+    bad = sm.make_args(4, 2)
+    bad.pos_tries = 0
+    _expect(call(1, bad), -1)
+    assert "pos_tries" in sm.last_error()
+    import torch
+    out = {k: torch.zeros(v, dtype=torch.int32) for k, v in
+           {"anchors": (4, 3), "relations": (4, 3), "positive": (4,), "negatives": (4, 2),
+            "n_valid": (4,), "pos_attempts": (4,), "neg_draws": (4,)}.items()}
+    with pytest.raises(ValueError, match="device tensor"):
+        sm.sample_negatives(None, dag, a, out, part=sm.NEG_CANDIDATES, workspace=sm.Workspace())
+    with pytest.raises(ValueError, match="explicit workspace"):
+        sm.sample_negatives(None, dag, a, out, part=sm.NEG_REST)
+
+
 def test_build_graph_validation_on_host(L):
     g = ctypes.c_void_p()
     tr = (ctypes.c_int32 * 3)(0, 0, 1)

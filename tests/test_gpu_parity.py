@@ -318,6 +318,76 @@ def test_accounting_variant_and_stage_split(qt):
     assert (st[:, 1] * 64 >= st[:, 0] // 8).all() and (st[:, 3] * 64 >= st[:, 2] // 8).all()
 
 
+@pytest.mark.parametrize("qt", sm.TYPES)
+def test_negatives_in_three_parts(qt):
+    # parts 0, 1, 2 in stream order equal one smore_sample_negatives call,
+    # rows and read accounting alike
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    dag = sm.query_preset(qt)
+    args = sm.make_args(300, 40, seed=6)
+    full = sm.alloc_outputs(300, 40)
+    sm.sample_positives(g, dag, args, full)
+    st_full = torch.zeros((300, 4), dtype=torch.int64, device="cuda")
+    sm.sample_negatives(g, dag, args, full, st_full)
+    out = {k: v.clone() for k, v in full.items()}
+    for k in ("negatives", "n_valid", "neg_draws"):
+        out[k].fill_(-7)
+    st = torch.zeros((300, 4), dtype=torch.int64, device="cuda")
+    ws = sm.Workspace()
+    for part in (sm.NEG_PREPARE, sm.NEG_CANDIDATES, sm.NEG_REST):
+        sm.sample_negatives(g, dag, args, out, st, part=part, workspace=ws)
+    a, b = to_numpy(full), to_numpy(out)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    assert torch.equal(st, st_full)
+
+
+def test_negatives_parts_across_streams():
+    # the benchmark's schedule: the candidate parts of several shapes back
+    # to back on one stream, preparation and the rest on each shape's own
+    # stream, ordered by events; rows equal those of plain calls
+    import torch
+    cfg, tr = config_graph("fb15k237")
+    g = sm.Graph(tr, cfg.n_entities, cfg.n_relations)
+    shapes = ["3p", "ip", "pi", "2in"]
+    args = sm.make_args(512, 64, seed=8)
+    ref, outs, wss, streams = {}, {}, {}, {}
+    for qt in shapes:
+        dag = sm.query_preset(qt)
+        ref[qt] = sm.alloc_outputs(512, 64)
+        sm.sample_positives(g, dag, args, ref[qt])
+        sm.sample_negatives(g, dag, args, ref[qt])
+        outs[qt] = {k: v.clone() for k, v in ref[qt].items()}
+        for k in ("negatives", "n_valid", "neg_draws"):
+            outs[qt][k].fill_(-7)
+        wss[qt] = sm.Workspace()
+        streams[qt] = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    cand = torch.cuda.Stream()
+    for rep in range(3):
+        for qt in shapes:
+            dag = sm.query_preset(qt)
+            sm.sample_negatives(g, dag, args, outs[qt], stream=streams[qt], part=sm.NEG_PREPARE,
+                                workspace=wss[qt])
+            prepared = torch.cuda.Event()
+            prepared.record(streams[qt])
+            cand.wait_event(prepared)
+            sm.sample_negatives(g, dag, args, outs[qt], stream=cand, part=sm.NEG_CANDIDATES,
+                                workspace=wss[qt])
+            drawn = torch.cuda.Event()
+            drawn.record(cand)
+            streams[qt].wait_event(drawn)
+            sm.sample_negatives(g, dag, args, outs[qt], stream=streams[qt], part=sm.NEG_REST,
+                                workspace=wss[qt])
+        torch.cuda.synchronize()
+        for qt in shapes:
+            a, b = to_numpy(ref[qt]), to_numpy(outs[qt])
+            for k in a:
+                assert np.array_equal(a[k], b[k]), (rep, qt, k)
+
+
 def test_negatives_on_caller_queries():
     # rows with an id out of range are skipped, the others verified
     import torch
