@@ -148,9 +148,9 @@ def test_graph_without_in_edges_of_depth():
     assert (got["n_valid"] == -1).all()
 
 
-@pytest.mark.parametrize("R", [8, 300])
+@pytest.mark.parametrize("R,inverse", [(8, False), (300, False), (300, True)])
 @pytest.mark.parametrize("qt", sm.TYPES)
-def test_two_level_in_edge_mask(qt, R):
+def test_two_level_in_edge_mask(qt, R, inverse):
     # more than 2^24 entities: the candidate kernel tests the coarse mask
     # (one bit per four entities), then the in-relation signature; 100,000
     # entities scattered over 20,000,000 ids hold every edge (with 300
@@ -160,7 +160,7 @@ def test_two_level_in_edge_mask(qt, R):
     ents = rng.choice(V, 100_000, replace=False).astype(np.int32)
     tr = np.stack([ents[rng.integers(0, len(ents), 400_000)], rng.integers(0, R, 400_000),
                    ents[rng.integers(0, len(ents), 400_000)]], axis=1).astype(np.int32)
-    g, og = graph_pair(tr, V, R)
+    g, og = graph_pair(tr, V, R, inverse)
     if R == 300:
         check_graph(g, og)
     for n_neg, nt in [(64, 256), (600, 2400)]:
