@@ -301,6 +301,8 @@ def main():
                     help="run the shapes of a step one after another on one stream "
                          "(default: one stream per shape; a shape's negatives start when the "
                          "previous shape's candidate kernel ends)")
+    ap.add_argument("--concurrent", action="store_true",
+                    help="no chain: the shapes' streams run each step without waiting for each other")
     ap.add_argument("--split", action="store_true",
                     help="candidate kernels of all shapes back to back on one stream "
                          "(smore_sample_negatives_part); the rest on each shape's stream")
@@ -454,7 +456,7 @@ def main():
             ev[qt][1].record(s)
         for qt in types:
             s = streams[qt]
-            if chain[0] is not None and s is not stream:
+            if chain[0] is not None and s is not stream and not args.concurrent:
                 if args.prepare_ahead:
                     sm.wait_before_kernel(chain[0])
                 else:
@@ -513,7 +515,7 @@ def main():
         a = acct[qt]
         # with --prepare-ahead the negative stage includes the wait for the
         # previous shape's candidate kernel: no per-shape rates then
-        rated = not (args.prepare_ahead or args.split)
+        rated = not (args.prepare_ahead or args.split or args.concurrent)
         per_type[qt] = {
             "queries_per_s": cfg.batch / ((pos + neg) / 1e3) if rated else None,
             "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3) if rated else None,
@@ -573,6 +575,7 @@ def main():
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed,
                    "streams": 1 if args.serial else len(types) + (1 if args.split else 0),
                    "schedule": "serial" if args.serial else "split" if args.split else
+                               "concurrent" if args.concurrent else
                                "chained, prepare ahead" if args.prepare_ahead else "chained"},
         "roofline": roofline,
         "cpu_baseline": cpu,
