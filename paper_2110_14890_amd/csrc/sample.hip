@@ -16,13 +16,17 @@
 // candidate draws; k_prepare once, then per round k_candidates, k_heavy
 // and the selection (k_compact_reg, or k_compact for long rounds), all on
 // the caller's stream with no host synchronisation in between (the kernels
-// themselves are described where they are defined).  Forward caching turns
+// themselves are described where they are defined).  The three steps can
+// also be launched apart (smore_sample_negatives_part): the preparation,
+// the first round's candidate kernel, the rest.  Forward caching turns
 // the anchors into their neighbour lists A_r(a) (sorted CSR groups, staged
 // in LDS when small, used in place when not); a draw without an in-edge is
-// settled by the in-edge mask (on large graphs a coarse mask first); the
-// others are verified backward from the candidate; the first occurrences
-// of the non-answers, in draw order, are the negatives, so the output is a
-// function of the draw indices alone.
+// settled by the in-edge mask (on large graphs a coarse mask, then the
+// entity's in-relation signature, which also settles draws with in-edges
+// under none of the root's relations); the others are verified backward
+// from the candidate; the first occurrences of the non-answers, in draw
+// order, are the negatives, so the output is a function of the draw
+// indices alone.
 //
 // Shared-candidate minibatches (smore_sample_shared) and verification of
 // caller candidates (smore_verify) run the same candidate and long-list
@@ -506,11 +510,13 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
 // --------------------------------------------------------------- negatives
 // Bidirectional rejection sampling of the negatives, in rounds of candidate
 // draws.  Per round:
-//   k_candidates  one wavefront per query: the round's draws, the in-edge
-//                 mask test, and for the survivors either a decision at lane
-//                 level or a push to the heavy queue;
-//   k_heavy       one wavefront per queued (query, draw): intersection of a
-//                 long backward list with the forward-cached list(s);
+//   k_candidates  one wavefront per query (one-wave workgroups): the round's
+//                 draws, the in-edge mask / signature test, and for the
+//                 survivors either a decision at lane level or a push to the
+//                 heavy queue;
+//   k_heavy       one wavefront per queued (query, draw), persistent
+//                 wavefronts: intersection of a long backward list with the
+//                 forward-cached list(s);
 //   k_compact_reg one wavefront per query (k_compact for rounds of more
 //                 than 1,024 draws): first-occurrence test of every draw so
 //                 far, ordered selection of the first n_neg kept.
