@@ -153,7 +153,8 @@ int smore_plan(const smore_query_dag *dag, int32_t tie_break, int32_t *cut_nodes
    and states, the queue of long intersections, the lists of queries still
    short of n_neg).  The caller allocates it; its contents need no
    initialisation and are scratch after the call.  Calls that may overlap on
-   the device must not share a workspace. */
+   the device must not share a workspace.  A call with n_neg = 0 draws no
+   candidates and needs no workspace (NULL and 0 are accepted). */
 int smore_sample_workspace_bytes(const smore_graph *g, const smore_query_dag *dag,
                                  const smore_sample_args *args, size_t *bytes);
 
@@ -250,7 +251,9 @@ typedef struct {
    (query_offset) draw different sets.  Every (query, member) pair is
    verified by the same bidirectional test as smore_sample.  Arguments,
    validation and workspace (smore_sample_workspace_bytes with the same
-   args) as for smore_sample; asynchronous on hip_stream. */
+   args) as for smore_sample; asynchronous on hip_stream.  With n_neg = 0
+   the set is empty (*n_shared = 0), no mask word exists, n_valid is 0 (or
+   -1 without a positive) and no workspace is needed. */
 int smore_sample_shared(const smore_graph *g, const smore_query_dag *dag,
                         const smore_sample_args *args, const smore_shared_out *out,
                         void *workspace, size_t ws_bytes, void *hip_stream);
@@ -271,7 +274,9 @@ int smore_sample_shared(const smore_graph *g, const smore_query_dag *dag,
    Candidates outside [0, V) are never negatives and read no graph data.
    args: batch = B, n_neg = n, neg_tries >= n (workspace sizing as for
    smore_sample, see smore_sample_workspace_bytes); the other fields are
-   checked as for smore_sample but unused.  Asynchronous on hip_stream. */
+   checked as for smore_sample but unused.  With n = 0 only n_valid is
+   written (0, or -1 as above) and candidates, mask and the workspace may
+   be NULL.  Asynchronous on hip_stream. */
 int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_sample_args *args,
                  const int32_t *anchors, const int32_t *relations, const int32_t *candidates,
                  uint32_t *mask, int32_t *n_valid, void *workspace, size_t ws_bytes,
@@ -282,8 +287,9 @@ int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_s
    stream immediately before and after one of its kernels in the first
    round of candidate draws: which = 0 the candidate kernel, 1 the kernel
    that intersects long lists, 2 the ordered selection.  One-shot: the
-   next call that reaches its kernel launches disarms it whether or not it
-   recorded.  Either event NULL disarms.  The events stay owned by the
+   next smore_sample, smore_sample_negatives or smore_sample_negatives_part
+   call of this thread disarms it whether or not it recorded, also when
+   that call fails validation.  Either event NULL disarms.  The events stay owned by the
    caller.  Returns SMORE_E_INVALID_ARG for another `which`. */
 int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
 
@@ -292,8 +298,9 @@ int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
    smore_sample or smore_sample_negatives call made by this thread makes its
    stream wait on the caller's HIP event (hipEvent_t) right before its
    first candidate kernel (which = 0), after the per-query preparation, so
-   the preparation does not wait.  One-shot: the next such call disarms it,
-   also when it launches no candidate kernel (n_neg = 0).  NULL disarms.
+   the preparation does not wait.  One-shot: the next such call (or
+   smore_sample_negatives_part) disarms it, also when it launches no
+   candidate kernel (n_neg = 0) or fails validation.  NULL disarms.
    The event stays owned by the caller.  SMORE_E_INVALID_ARG for another
    `which`; SMORE_E_HIP if the wait cannot be enqueued (the call then
    launches nothing after the preparation). */

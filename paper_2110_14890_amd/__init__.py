@@ -220,6 +220,8 @@ def _workspace(ws, dag, args, stream=None):
     """The caller's workspace, or a default one per (device, stream) the call
     runs on, so that calls on different streams never share scratch."""
     import torch
+    if args.n_neg == 0:        # nothing is drawn: the library needs no workspace
+        return None, 0
     if ws is None:
         st = stream if stream is not None else torch.cuda.current_stream()
         key = (st.device, st.cuda_stream)

@@ -508,6 +508,15 @@ int run_sample(const smore_graph* g, const smore_query_dag* dag, const smore_sam
                const smore_sample_out* out, int64_t* stats, void* workspace, size_t ws_bytes,
                void* hip_stream, int stages, int parts = smore::NEG_ALL)
 {
+    // the one-shot instrumentation arms belong to this call whatever its
+    // outcome: a call that fails validation disarms them too
+    struct Disarm {
+        bool on;
+        ~Disarm()
+        {
+            if (on) smore::disarm();
+        }
+    } disarm_on_return{(stages & NEG) != 0};
     // host-side checks first (they need no device), the graph last
     if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
     int qt = -1;
@@ -560,7 +569,7 @@ int smore_verify(const smore_graph* g, const smore_query_dag* dag, const smore_s
         return fail(SMORE_E_INVALID_ARG, "an input or output pointer is NULL");
     if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
     const smore::SampleParams p = params_of(a);
-    if (!workspace || ws_bytes < smore::negatives_workspace_bytes(p))
+    if (a->n_neg > 0 && (!workspace || ws_bytes < smore::negatives_workspace_bytes(p)))
         return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
                     smore::negatives_workspace_bytes(p));
     const char* err = "";
@@ -583,7 +592,7 @@ int smore_sample_shared(const smore_graph* g, const smore_query_dag* dag, const 
         return fail(SMORE_E_INVALID_ARG, "an output pointer is NULL");
     if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
     const smore::SampleParams p = params_of(a);
-    if (!workspace || ws_bytes < smore::negatives_workspace_bytes(p))
+    if (a->n_neg > 0 && (!workspace || ws_bytes < smore::negatives_workspace_bytes(p)))
         return fail(SMORE_E_INVALID_ARG, "workspace missing or smaller than %zu bytes",
                     smore::negatives_workspace_bytes(p));
     // positives exactly as smore_sample (same draws), into the shared outputs

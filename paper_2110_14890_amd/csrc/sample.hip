@@ -38,6 +38,7 @@
 #include <cstring>
 
 #include "philox.h"
+#include "rows.h"
 #include "smore_internal.h"
 
 namespace smore {
@@ -966,7 +967,6 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
         ws.ctrl[3] = 0;
     }
     int32_t anc[3], rel[3];
-    int32_t* row = out.negatives + (int64_t)b * p.n_neg;
     int32_t* q = ws.qf + (int64_t)b * QF;
     if (f == 0) {
         ws.act[0][b] = b;
@@ -975,19 +975,8 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
     }
     if (!query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel)) {
         if (f == 0) {
-            if (!p.shared_mode) {   // a shared-candidate minibatch has no per-query rows
-                for (int32_t k = 0; k < p.n_neg; ++k) row[k] = -1;
-                out.neg_draws[b] = -1;
-            }
-            out.n_valid[b] = -1;
+            write_undrawn_row(p, out, b, false);
             q[6] = -1;   // skipped by the rounds
-        }
-        return;
-    }
-    if (p.n_neg == 0) {
-        if (f == 0) {
-            out.n_valid[b] = 0;
-            if (!p.shared_mode) out.neg_draws[b] = 0;
         }
         return;
     }
@@ -1023,6 +1012,22 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
             stats[4 * (int64_t)b + 1] = (int64_t)y;
         }
     }
+}
+
+// Calls with n_neg = 0 draw nothing: one thread per query writes its
+// n_valid (0, or -1 for a skipped query), and for per-query sampling its
+// draw count.  No workspace is read or written.
+template <int QT>
+__global__ __launch_bounds__(256) void k_no_draws(GraphView g, SampleParams p, smore_sample_out out,
+                                                  int64_t* stats, int32_t R)
+{
+    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= p.batch) return;
+    int32_t anc[3], rel[3];
+    const bool ok = query_ok(g, out, b, Shape<QT>::n_anc, Shape<QT>::n_rel, R, anc, rel);
+    write_undrawn_row(p, out, b, ok);
+    if (stats)
+        for (int k = 0; k < 4; ++k) stats[4 * (int64_t)b + k] = 0;
 }
 
 // One wavefront per active query, in one-wave workgroups: a workgroup per
@@ -1576,11 +1581,15 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                   int64_t* stats, int32_t R, int parts, hipStream_t st, const char** err)
 {
     int rc;
+    if (p.n_neg == 0) {   // nothing to draw: no preparation, no workspace
+        if (!(parts & NEG_PREPARE)) return SMORE_OK;
+        k_no_draws<QT><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, out, stats, R);
+        return check_launch(err);
+    }
     if (parts & NEG_PREPARE) {
         k_prepare<QT, T><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, out, ws, stats, R);
         if ((rc = check_launch(err))) return rc;
     }
-    if (p.n_neg == 0) return SMORE_OK;
     const int rounds = n_rounds(p);
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
@@ -1770,9 +1779,12 @@ int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out
               uint32_t* mask, int32_t R, hipStream_t st, const char** err)
 {
     int rc;
+    if (p.n_neg == 0) {   // no candidates: n_valid only (0, or -1 for a skipped query)
+        k_no_draws<QT><<<(p.batch + 255) / 256, 256, 0, st>>>(gv, p, q, nullptr, R);
+        return check_launch(err);
+    }
     k_prepare<QT, NoTally><<<(p.batch + 63) / 64, 256, 0, st>>>(gv, p, q, ws, nullptr, R);
     if ((rc = check_launch(err))) return rc;
-    if (p.n_neg == 0) return SMORE_OK;
     k_candidates<QT, NoTally, true><<<max(p.batch, 1), CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
                                                                      p.n_neg);
     if ((rc = check_launch(err))) return rc;
@@ -1826,6 +1838,12 @@ GraphView view_of(const smore_graph* g)
 
 void arm_wait(void* event) { g_wait = (hipEvent_t)event; }
 
+void disarm()
+{
+    g_prof = ProfileArm{};
+    g_wait = nullptr;
+}
+
 void arm_profile(void* start_event, void* stop_event, int which)
 {
     g_prof.start = (hipEvent_t)start_event;
@@ -1855,16 +1873,13 @@ int launch_negative(const smore_graph* g, QType qt, const SampleParams& p,
 {
     Ws ws;
     const size_t need = ws_layout(p, &ws, (char*)workspace);
-    if (!workspace || ws_bytes < need) {
+    if (p.n_neg > 0 && (!workspace || ws_bytes < need)) {
         *err = "workspace too small (see smore_sample_workspace_bytes)";
         return SMORE_E_INVALID_ARG;
     }
     const GraphView gv = view_of(g);
-    const int rc = stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, parts, st, err)
-                         : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, parts, st, err);
-    g_prof = ProfileArm{};  // one-shot: an arm never outlives the call it was meant for
-    g_wait = nullptr;
-    return rc;
+    return stats ? dispatch_negatives<Tally>(qt, gv, p, out, ws, stats, g->R, parts, st, err)
+                 : dispatch_negatives<NoTally>(qt, gv, p, out, ws, nullptr, g->R, parts, st, err);
 }
 
 int launch_shared(const smore_graph* g, QType qt, const SampleParams& p0, const smore_sample_out& pos,
@@ -1878,13 +1893,15 @@ int launch_shared(const smore_graph* g, QType qt, const SampleParams& p0, const 
     p.cand_stride = 0;
     Ws ws;
     const size_t need = ws_layout(p, &ws, (char*)workspace);
-    if (!workspace || ws_bytes < need) {
+    if (p.n_neg > 0 && (!workspace || ws_bytes < need)) {
         *err = "workspace too small (see smore_sample_workspace_bytes)";
         return SMORE_E_INVALID_ARG;
     }
     const GraphView gv = view_of(g);
     const int rc = draw_shared_set(p, gv.V, shared, n_shared, st, err);
-    if (rc) return rc;
+    // an empty set leaves nothing to verify: the positives' n_valid (0, or -1
+    // without a positive) is the row count, and no mask word exists
+    if (rc || p.n_neg == 0) return rc;
     return dispatch_pairs(qt, gv, p, pos, ws, mask, g->R, st, err);
 }
 
@@ -1900,7 +1917,7 @@ int launch_verify(const smore_graph* g, QType qt, const SampleParams& p0, const 
     p.cand_stride = p.n_neg;
     Ws ws;
     const size_t need = ws_layout(p, &ws, (char*)workspace);
-    if (!workspace || ws_bytes < need) {
+    if (p.n_neg > 0 && (!workspace || ws_bytes < need)) {
         *err = "workspace too small (see smore_sample_workspace_bytes)";
         return SMORE_E_INVALID_ARG;
     }

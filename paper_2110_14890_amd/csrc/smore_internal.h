@@ -124,6 +124,8 @@ int launch_verify(const smore_graph* g, QType qt, const SampleParams& p, const i
 void arm_profile(void* start_event, void* stop_event, int which);
 // one-shot wait on an event before the first candidate kernel of the next negatives call
 void arm_wait(void* event);
+// clear both one-shot arms of the calling thread
+void disarm();
 int64_t gather_probe_threads(int64_t n_reads);
 int launch_gather_probe(const void* table, int64_t table_bytes, int64_t n_reads, uint32_t* sink,
                         hipStream_t st, const char** err);

@@ -76,10 +76,13 @@ def test_shared_budget_and_pathless_graphs():
         assert_shared_same(got, ref, f"pathless {qt}")
 
 
-@pytest.mark.skip(reason="an empty shared set faulted the GPU: k_prepare took a NULL set pointer for "
-                         "per-query mode and wrote the absent per-query draw counts; fixed with an "
-                         "explicit shared-mode flag, not yet run on a GPU")
 def test_shared_empty_set():
+    """An empty shared set (n_neg = 0): the set pointer, the mask and the
+    workspace are NULL.  Such a call once wrote per-query draw counts through
+    the NULL pointer (per-query mode was inferred from a NULL set); it now
+    draws the empty set and launches no per-query negatives kernel, and the
+    host-side rows of such calls run under the address sanitizer on the CPU
+    (tests/test_host_sanitized.py)."""
     require_gpu()
     rng = np.random.default_rng(3)
     tr = kgsynth.random_tiny(rng, 40, 2, 500)

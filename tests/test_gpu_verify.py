@@ -69,3 +69,24 @@ def test_evaluation_on_nested_graphs():
         # answers missing from G_valid are missing from G_train too
         assert (hard["train"][ok] >= hard["valid"][ok]).all()
         assert hard["train"][ok].any()
+
+
+def test_verify_and_sample_without_candidates():
+    """n = 0 candidates per query: smore_verify writes only n_valid (0, or
+    -1 for a query with an out-of-range anchor), and smore_sample with
+    n_neg = 0 writes n_valid and neg_draws = 0 (or -1 without a positive);
+    neither needs a workspace (the binding passes NULL)."""
+    require_gpu()
+    rng = np.random.default_rng(41)
+    tr = kgsynth.random_tiny(rng, 500, 4, 6000)
+    g, og = graph_pair(tr, 500, 4, True)
+    for qt in sm.TYPES:
+        progress(f"no candidates {qt}")
+        q = og.sample(qt, 64, 0, seed=2, neg_tries=0)
+        anchors, relations = q["anchors"].copy(), q["relations"].copy()
+        anchors[3] = 900
+        mask, nv = gpu_verify(g, qt, anchors, relations, np.zeros((64, 0), np.int32))
+        ref = og.verify(qt, anchors, relations, np.zeros((64, 0), np.int32))
+        assert mask.size == 0 and np.array_equal(nv, ref["n_valid"]), qt
+        got = gpu_sample(g, qt, 64, 0, seed=2, neg_tries=0)
+        assert_same(got, og.sample(qt, 64, 0, seed=2, neg_tries=0), what=f"{qt} n_neg 0")
