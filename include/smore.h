@@ -181,6 +181,26 @@ int smore_sample_workspace_bytes(const smore_graph *g, const smore_query_dag *da
 int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_sample_args *args,
                  const smore_sample_out *out, void *workspace, size_t ws_bytes, void *hip_stream);
 
+/* smore_sample for callers that cannot allocate device memory (code under
+   HIP graph capture, tight serving loops, harnesses that forbid
+   allocation): the same arguments, validation, outputs and stream
+   semantics, but no workspace argument.  The scratch is a fixed array of
+   SMORE_NOALLOC_SCRATCH_BYTES in device memory, one per GPU the library
+   runs on, held until the process ends; the call itself allocates and
+   frees nothing.  Every call on one GPU shares that array, so calls that
+   may overlap on a GPU (different streams, different threads) race and
+   must be serialised by the caller; the array keeps the last call's
+   contents, and each call initialises whatever it reads.  Errors as for
+   smore_sample, and SMORE_E_UNSUPPORTED when the arguments need more
+   scratch than the fixed size (smore_sample_workspace_bytes gives the
+   need; about 22 KB per query at 512 negatives and 2,048 draws, e.g.
+   2,048 such queries, or 16,384 queries with 64 negatives and 256
+   draws). */
+#define SMORE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int smore_sample_noalloc(const smore_graph *g, const smore_query_dag *dag,
+                         const smore_sample_args *args, const smore_sample_out *out,
+                         void *hip_stream);
+
 /* The two stages of smore_sample, for callers that time or feed them
    separately.  Same arguments and validation as smore_sample.
    smore_sample_positives writes anchors, relations, positive, pos_attempts

@@ -85,6 +85,8 @@ def lib() -> ctypes.CDLL:
                                                    ctypes.POINTER(ctypes.c_size_t)]
         L.smore_sample.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
                                    ctypes.POINTER(SampleOut), c_vp, ctypes.c_size_t, c_vp]
+        L.smore_sample_noalloc.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
+                                           ctypes.POINTER(SampleOut), c_vp]
         L.smore_sample_shared.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs),
                                           ctypes.POINTER(SharedOut), c_vp, ctypes.c_size_t, c_vp]
         L.smore_verify.argtypes = [c_vp, ctypes.POINTER(QueryDag), ctypes.POINTER(SampleArgs), c_vp,
@@ -237,6 +239,19 @@ def sample_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict, stream
     wp, wn = _workspace(workspace, dag, args, stream)
     _check(lib().smore_sample(graph.handle, ctypes.byref(dag), ctypes.byref(args),
                               ctypes.byref(_out_struct(out)), wp, wn, _stream_handle(stream)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def sample_noalloc_into(graph: Graph, dag: QueryDag, args: SampleArgs, out: dict,
+                        stream=None) -> dict:
+    """smore_sample_noalloc: smore_sample without a workspace argument (the
+    library's fixed per-device scratch; calls on one GPU must not overlap)."""
+    _require(out, _sample_shapes(args))
+    _check(lib().smore_sample_noalloc(graph.handle, ctypes.byref(dag), ctypes.byref(args),
+                                      ctypes.byref(_out_struct(out)), _stream_handle(stream)))
     return out
 
 

@@ -615,6 +615,32 @@ int smore_sample_shared(const smore_graph* g, const smore_query_dag* dag, const 
     return ok();
 }
 
+int smore_sample_noalloc(const smore_graph* g, const smore_query_dag* dag, const smore_sample_args* a,
+                         const smore_sample_out* out, void* hip_stream)
+{
+    if (!a || !out) return fail(SMORE_E_INVALID_ARG, "args or out is NULL");
+    int qt = -1;
+    int rc = check_args(dag, a, &qt);
+    if (rc) return rc;
+    const smore::SampleParams p = params_of(a);
+    const size_t need = a->n_neg > 0 ? smore::negatives_workspace_bytes(p) : 0;
+    if (need > (size_t)SMORE_NOALLOC_SCRATCH_BYTES)
+        return fail(SMORE_E_UNSUPPORTED,
+                    "smore_sample_noalloc: these arguments need %zu bytes of scratch, more than its "
+                    "fixed %zu; use smore_sample with a caller workspace",
+                    need, (size_t)SMORE_NOALLOC_SCRATCH_BYTES);
+    // the graph's device must be current: the scratch taken is that device's
+    if ((rc = check_graph_and_cut(g, dag, qt))) return rc;
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    if (need) {
+        const char* err = "";
+        if ((rc = smore::scratch_workspace(&ws, &ws_bytes, &err)))
+            return fail(rc, "smore_sample_noalloc: %s", err);
+    }
+    return run_sample(g, dag, a, out, nullptr, ws, ws_bytes, hip_stream, POS | NEG);
+}
+
 int smore_sample_positives(const smore_graph* g, const smore_query_dag* dag,
                            const smore_sample_args* a, const smore_sample_out* out, void* hip_stream)
 {

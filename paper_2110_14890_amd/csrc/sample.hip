@@ -36,6 +36,7 @@
 
 #include <climits>
 #include <cstring>
+#include <mutex>
 
 #include "philox.h"
 #include "rows.h"
@@ -1835,6 +1836,39 @@ GraphView view_of(const smore_graph* g)
 }
 
 }  // namespace
+
+// Workspace of smore_sample_noalloc: a fixed array in device memory, one
+// copy per GPU the library runs on, held until the process ends.  Host code
+// never uses the array's name as an address: each device's address comes
+// from hipGetSymbolAddress, taken once per device with that device current.
+namespace {
+static __device__ __align__(256) char scratch[SMORE_NOALLOC_SCRATCH_BYTES];
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES];
+}  // namespace
+
+int scratch_workspace(void** ptr, size_t* bytes, const char** err)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) {
+        *err = "no usable current device for the fixed scratch";
+        return SMORE_E_HIP;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            *err = e != hipSuccess ? hipGetErrorString(e) : "scratch has no device address";
+            return SMORE_E_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    *bytes = SMORE_NOALLOC_SCRATCH_BYTES;
+    return SMORE_OK;
+}
 
 void arm_wait(void* event) { g_wait = (hipEvent_t)event; }
 

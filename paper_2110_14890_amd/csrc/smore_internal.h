@@ -126,6 +126,8 @@ void arm_profile(void* start_event, void* stop_event, int which);
 void arm_wait(void* event);
 // clear both one-shot arms of the calling thread
 void disarm();
+// the current device's fixed scratch (SMORE_NOALLOC_SCRATCH_BYTES bytes)
+int scratch_workspace(void** ptr, size_t* bytes, const char** err);
 int64_t gather_probe_threads(int64_t n_reads);
 int launch_gather_probe(const void* table, int64_t table_bytes, int64_t n_reads, uint32_t* sink,
                         hipStream_t st, const char** err);

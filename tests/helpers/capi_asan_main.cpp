@@ -171,6 +171,16 @@ static void validation()
     CHECK(smore_verify(nullptr, &d, &a, dummy, dummy, nullptr, nullptr, dummy, dummy, 8, nullptr) ==
           SMORE_E_INVALID_ARG);
     CHECK(std::strstr(smore_last_error(), "pointer") != nullptr);
+    // the entry point without a workspace refuses arguments that need more
+    // than its fixed scratch before it looks at the graph
+    b = a;
+    b.batch = 16384;
+    b.n_neg = 512;
+    b.neg_tries = 2048;
+    CHECK(smore_sample_noalloc(nullptr, &d, &b, &o, nullptr) == SMORE_E_UNSUPPORTED);
+    CHECK(std::strstr(smore_last_error(), "scratch") != nullptr);
+    CHECK(smore_sample_noalloc(nullptr, &d, &a, &o, nullptr) == SMORE_E_INVALID_ARG);
+    CHECK(std::strstr(smore_last_error(), "graph") != nullptr);
     // probe argument checks
     uint32_t sink[4];
     CHECK(smore_gather_probe(nullptr, 64, 1, sink, 4, nullptr) == SMORE_E_INVALID_ARG);
