@@ -12,7 +12,22 @@ relations, 338M distinct triples, rank-Zipf(1.3) endpoints sharing one
 permutation, rank-Zipf(1.0) relations), shapes 3p/ip/pi, batch 16,384,
 512 negatives, 2,048 candidate draws per query, seed 0.
 
+Each timed step samples a new batch (query ids advance by the batch size),
+so no step re-reads lines a previous identical step left in the caches.
+
 Printed: one JSON line on stdout.  Progress goes to stderr.
+
+Roofline.  The algorithmic bytes of a launch come from the oracle, not from
+the kernels: oracle_verify_lines counts, per query, the distinct 64-byte
+lines of the device layout a bidirectional check under the strict node cut
+reads for the first round's candidate draws (forward caching, each
+candidate's node entries and group search, backward lists), split into the
+part a first verification pass makes and the part below long lists or
+forward sets too large to stage.  `roofline` is for the longest kernel of
+the step by event time; `kernels` gives every candidate and long-list
+kernel beside it with the same accounting, the kernels' own read tally and,
+when the committed counter summary matches the current sources, the HBM
+traffic rocprofv3 measured.
 """
 from __future__ import annotations
 
@@ -33,19 +48,69 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def host_threads():
+    """Threads the oracle uses: the host CPUs this process may run on, or
+    fewer when OMP_NUM_THREADS sets the job's CPU share."""
+    visible = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS") or 0)
+    return (min(share, visible) if share > 0 else visible), visible
+
+
+def sample_hip_sha():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2110_14890_amd", "csrc", "sample.hip")
+    with open(src, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def first_round_draws(n_neg, neg_tries):
+    """Candidate draws of the first round of smore_sample_negatives: n_neg
+    plus a margin of n_neg / 32 + 8, at most neg_tries."""
+    return min(n_neg + n_neg // 32 + 8, neg_tries)
+
+
+def oracle_lines(og, cfg, types, neg_tries, threads):
+    """Algorithmic bytes of the first round's verification, per shape, from
+    the oracle: positives of the benchmark's first batch (query ids
+    0 .. batch-1) by the oracle's own reverse sampling, then
+    oracle_verify_lines under the strict node cut (oracle/cuts.py) for the
+    first round's draws.  Lines x 64 B; part 0 = the first verification
+    pass (the candidate kernel's share), part 1 = long lists and unstaged
+    forward sets (the long-list kernel's share)."""
+    from oracle import cuts
+
+    res = {}
+    j0 = first_round_draws(cfg.n_neg, neg_tries)
+    for qt in types:
+        t = time.time()
+        q = og.sample(qt, cfg.batch, 0, seed=cfg.seed, threads=threads)
+        op, ch, _, root = __import__("oracle").type_plan(qt)
+        mask = cuts.mask(cuts.strict(op, ch, root))
+        L = og.verify_lines(qt, q["anchors"], q["relations"], q["positive"], mask, cfg.seed, 0, j0,
+                            threads=threads)
+        valid = q["positive"] >= 0
+        res[qt] = {"queries": int(valid.sum()), "draws_per_query": j0,
+                   "cut_nodes": sorted(cuts.strict(op, ch, root)),
+                   "part0_bytes": int(L[valid, 0].sum()) * 64,
+                   "part1_bytes": int(L[valid, 1].sum()) * 64,
+                   "total_bytes": int(L[valid, 2].sum()) * 64,
+                   "seconds": round(time.time() - t, 2)}
+        log(f"oracle lines {qt}: {res[qt]}")
+    return res
+
+
 def workload_name(cfg, types):
     return (f"{cfg.name}-shaped synthetic KG: {cfg.n_entities:,} entities, "
             f"{cfg.n_relations:,} relations, {cfg.n_triples:,} triples; "
             f"{'/'.join(types)} batch {cfg.batch:,}, {cfg.n_neg} negatives")
 
 
-def traffic_for(kernel):
+def traffic_for(config, kernel):
     """HBM bytes per launch of `kernel` (e.g. "k_candidates<3p> r0") from the
-    committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE scaled by
-    a plain copy's readings), or None when there is none or it was taken on
-    other sources of the sampling kernels."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "negatives_freebase_hbm_bytes.txt")
+    committed rocprofv3 counter summary of the workload (FETCH_SIZE and
+    WRITE_SIZE scaled by a plain copy's readings), or None when there is
+    none or it was taken on other sources of the sampling kernels."""
+    path = os.path.join(ROOT, "profiles", f"negatives_{config}_hbm_bytes.txt")
     if not os.path.exists(path):
         return None
     fields, kernels = {}, {}
@@ -59,10 +124,7 @@ def traffic_for(kernel):
                 kernels[parts[0]] = int(parts[-1].split()[-1])
             else:
                 fields[key.strip()] = val.strip()
-    src = os.path.join(ROOT, "paper_2110_14890_amd", "csrc", "sample.hip")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    if fields.get("sample_hip_sha256_16") != sha:
+    if fields.get("sample_hip_sha256_16") != sample_hip_sha():
         return None
     return kernels.get(kernel)
 
@@ -247,17 +309,11 @@ def verify_bench(cfg, g, types, steps, warmup, stream):
                           "complete_queries": int((nv == n_cand).sum().item())}), flush=True)
 
 
-def cpu_baseline(cfg, triples, types, seconds, threads):
+def cpu_baseline(cfg, og, types, seconds, threads, visible):
     """The CPU oracle, timed on the host on the first queries of each shape
-    (a bounded sample of the same workload)."""
-    import numpy as np
-    import oracle
-
-    t0 = time.time()
-    og = oracle.Graph(triples, cfg.n_entities, cfg.n_relations, cfg.add_inverse, threads=threads)
-    log(f"oracle graph built in {time.time() - t0:.1f} s")
+    (a bounded sample of the same workload), on every CPU the job has."""
     per_type = seconds / len(types)
-    done, spent, rows = 0, 0.0, {}
+    done, spent, rows, rates = 0, 0.0, {}, {}
     for qt in types:
         n, t_type, chunk = 0, 0.0, threads
         while t_type < per_type and n < cfg.batch:
@@ -269,14 +325,172 @@ def cpu_baseline(cfg, triples, types, seconds, threads):
             n += c
             chunk = min(chunk * 2, 8 * threads)
         rows[qt] = n
+        rates[qt] = round(n / t_type, 2)
         done += n
         spent += t_type
         log(f"oracle {qt}: {n} queries in {t_type:.1f} s")
-    del og
     sample = ", ".join(f"{qt}: first {rows[qt]}" for qt in types)
     return {"value": done / spent, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "host_cpus_visible": visible,
+            "per_type_queries_per_s": rates,
             "sample": f"{sample} queries of the benchmark batch (same graph, seed, n_neg); "
-                      f"{spent:.1f} s of oracle sampling, adjacency build not timed"}
+                      f"{spent:.1f} s of oracle sampling, adjacency build not timed; "
+                      f"{threads} threads (the job's CPU share; {visible} CPUs visible)"}
+
+
+SHAPES = ("1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up", "2in", "3in", "inp", "pin", "pni")
+GRAPH_BUILD_KERNELS = ("k_radix", "k_scan", "k_add", "k_flag", "k_write_g", "k_node", "k_compact3",
+                       "k_load", "k_has_in", "k_compact_active", "k_sig")
+
+
+def profile_commands(config, steps):
+    cfgflag = "" if config == "freebase" else f" --config {config}"
+    run = f"python3 -u bench.py{cfgflag} --no-cpu-baseline --no-gather-ceiling --no-oracle-lines"
+    d = f"gpurun_out/prof_{config}"
+    return [
+        f"mkdir -p {d}/trace",
+        f"rocprofv3 --kernel-trace --stats -d {d}/trace -o bench --output-format csv -- {run} "
+        f"--steps {steps} --warmup 3 > {d}/trace/bench.log",
+        f"rocprofv3 --pmc FETCH_SIZE -d {d}/fetch -o bench --output-format csv -- {run} --steps 3 --warmup 1",
+        f"rocprofv3 --pmc WRITE_SIZE -d {d}/write -o bench --output-format csv -- {run} --steps 3 --warmup 1",
+        f"rocprofv3 --pmc FETCH_SIZE -d {d}/copy_fetch -o copy --output-format csv -- "
+        "python3 -u bench.py --copy-calibration 1024",
+        f"rocprofv3 --pmc WRITE_SIZE -d {d}/copy_write -o copy --output-format csv -- "
+        "python3 -u bench.py --copy-calibration 1024",
+    ]
+
+
+def summarize_profiles(config, folder, steps):
+    """Write profiles/negatives_<config>_trace_and_counters.md and
+    profiles/negatives_<config>_hbm_bytes.txt from the rocprofv3 output of
+    the commands profile_commands() lists (kernel trace, then FETCH_SIZE and
+    WRITE_SIZE passes of the benchmark and of a 1 GiB copy)."""
+    import csv
+    import glob
+    import re
+    import statistics
+    from collections import defaultdict
+
+    def one(pattern):
+        got = sorted(glob.glob(os.path.join(folder, pattern), recursive=True))
+        if not got:
+            raise SystemExit(f"summarize: nothing matches {pattern} under {folder}")
+        return got[0]
+
+    def kname(n):
+        m = re.search(r"(k_\w+)(?:<([^>]*)>)?", n)
+        if not m:
+            return None
+        k, targs = m.group(1), m.group(2)
+        if k.startswith(GRAPH_BUILD_KERNELS) or not targs:
+            return k
+        parts = [x.strip() for x in targs.split(",")]
+        if k in ("k_compact_reg", "k_positive"):   # templated on a count, not a shape
+            return f"{k}<{parts[0]}>"
+        qt = SHAPES[int(parts[0])] if parts[0].isdigit() else parts[0]
+        acct = any("Tally" in x and "NoTally" not in x for x in parts)
+        shared = any(x == "true" for x in parts)
+        return f"{k}<{qt}{', accounting' if acct else ''}{', given candidates' if shared else ''}>"
+
+    def tagged(rows):
+        out, rnd = [], defaultdict(lambda: -1)
+        for r in sorted(rows, key=lambda r: int(r["Dispatch_Id"])):
+            n = kname(r["Kernel_Name"])
+            if n is None:
+                continue
+            shape = n[n.index("<") + 1:].split(",")[0].rstrip(">") if "<" in n else None
+            if n.startswith(("k_prepare", "k_no_draws")):
+                rnd[shape] = -1
+            if n.startswith("k_candidates"):
+                rnd[shape] += 1
+            rr = rnd[shape] if n.startswith(("k_candidates", "k_heavy")) else None
+            out.append((n, rr, r))
+        return out
+
+    trace = list(csv.DictReader(open(one("**/*kernel_trace.csv"))))
+    dur = defaultdict(list)
+    for n, rr, r in tagged(trace):
+        dur[(n, rr)].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    bench_line = None
+    for ln in open(one("**/bench.log")):
+        if ln.startswith('{"metric"'):
+            bench_line = json.loads(ln)
+    ctr = {}
+    for c in ("fetch", "write"):
+        a = defaultdict(list)
+        for n, rr, r in tagged(list(csv.DictReader(open(one(f"{c}/**/*counter_collection.csv"))))):
+            a[(n, rr)].append(float(r["Counter_Value"]))
+        ctr[c] = {k: sum(v) / len(v) for k, v in a.items()}
+    cal = {}
+    for c in ("fetch", "write"):
+        rows = [r for r in csv.DictReader(open(one(f"copy_{c}/**/*counter_collection.csv")))
+                if "copyBuffer" in r["Kernel_Name"]]
+        kib = statistics.mean(float(r["Counter_Value"]) for r in rows)
+        cal[c] = (kib, (1 << 20) / kib)      # a 1 GiB copy moves 1,048,576 KiB each way
+    sha = bench_line["config"].get("sample_hip_sha256_16") if bench_line else None
+    keep = [k for k in dur if not k[0].startswith(GRAPH_BUILD_KERNELS)]
+    build = [k for k in dur if k[0].startswith(GRAPH_BUILD_KERNELS)]
+    L = [f"# Kernel trace and HBM counters: negative sampling, {config}-shaped workload\n",
+         f"Workload: {bench_line['config']['workload'] if bench_line else config}; "
+         f"{bench_line['config']['neg_tries'] if bench_line else '?'} candidate draws per query; "
+         "each step samples a new batch of query ids.\n",
+         f"Profiled sources: `paper_2110_14890_amd/csrc/sample.hip` sha256 prefix `{sha}`.\n",
+         "Commands (from the repository root after `cd /tmp && export TMPDIR=/tmp`, each a separate "
+         "process), then `python3 bench.py --summarize " + f"gpurun_out/prof_{config}"
+         + ("" if config == "freebase" else f" --config {config}") + "` to write this file:\n", "```"]
+    L += profile_commands(config, steps) + ["```\n"]
+    L.append("Kernels are grouped by name and, for the candidate and long-list kernels, by round of "
+             "candidate draws (round 0 covers the first n_neg + n_neg / 32 + 8 draws). "
+             "\"accounting\" rows are the one untimed pass with the kernels' own read tally.\n")
+    L += ["## Durations (kernel trace, all launches of the run)\n",
+          "| kernel | round | launches | avg us | median us | total ms |", "|---|---|---|---|---|---|"]
+    for k in sorted(keep, key=lambda k: -sum(dur[k])):
+        v = dur[k]
+        L.append("| %s | %s | %d | %.1f | %.1f | %.2f |" % (k[0], "" if k[1] is None else k[1], len(v),
+                                                          sum(v) / len(v), statistics.median(v),
+                                                          sum(v) / 1e3))
+    L.append("\nOne-time graph build in the same run (not timed by the benchmark): %d launches, "
+             "%.1f ms in total.\n" % (sum(len(dur[k]) for k in build), sum(sum(dur[k]) for k in build) / 1e3))
+    if bench_line:
+        L.append(f"Benchmark figures of the traced run: {bench_line['value']:,.0f} queries/s, "
+                 f"{bench_line['ms_per_step']} ms per step.\n")
+        L.append("Agreement with the benchmark's event timing (HIP events the library records around "
+                 "the launch on its stream), average over the timed steps:\n")
+        L += ["| kernel | events (ms) | trace avg (ms) |", "|---|---|---|"]
+        for kr in bench_line.get("kernels", []):
+            base, rd = kr["kernel"].split(" r")
+            tr_ = dur.get((base, int(rd)))
+            L.append("| %s | %.4f | %s |" % (kr["kernel"], kr["avg_launch_ms"],
+                                             "%.4f" % (sum(tr_) / len(tr_) / 1e3) if tr_ else "-"))
+        L.append("")
+    L += ["## HBM counters (KiB per dispatch, averaged over the launches of each group)\n",
+          "Calibration: a plain device copy of 1 GiB reads %.1f KiB of FETCH_SIZE and %.1f KiB of "
+          "WRITE_SIZE per launch for 1,048,576 KiB moved each way, so FETCH_SIZE is scaled by %.3f "
+          "and WRITE_SIZE by %.3f below.\n" % (cal["fetch"][0], cal["write"][0], cal["fetch"][1],
+                                               cal["write"][1]),
+          "| kernel | round | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled HBM bytes per launch |",
+          "|---|---|---|---|---|"]
+    txt = []
+    for k in sorted(keep, key=lambda k: -sum(dur[k])):
+        if k not in ctr["fetch"]:
+            continue
+        f, w = ctr["fetch"][k], ctr["write"].get(k, 0.0)
+        hb = f * 1024 * cal["fetch"][1] + w * 1024 * cal["write"][1]
+        L.append("| %s | %s | %.1f | %.1f | %.4g |" % (k[0], "" if k[1] is None else k[1], f, w, hb))
+        if k[1] in (0, None) and "accounting" not in k[0]:
+            txt.append("kernel: %s | fetch_kib %.1f | write_kib %.1f | hbm_bytes_per_launch %d"
+                       % (k[0] + ("" if k[1] is None else " r%d" % k[1]), f, w, hb))
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    md = os.path.join(ROOT, "profiles", f"negatives_{config}_trace_and_counters.md")
+    with open(md, "w") as fh:
+        fh.write("\n".join(L) + "\n")
+    head = [f"# HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (KiB per dispatch), "
+            f"{config}-shaped workload; commands in negatives_{config}_trace_and_counters.md",
+            f"sample_hip_sha256_16: {sha}", "fetch_scale: %.4f" % cal["fetch"][1],
+            "write_scale: %.4f" % cal["write"][1]]
+    with open(os.path.join(ROOT, "profiles", f"negatives_{config}_hbm_bytes.txt"), "w") as fh:
+        fh.write("\n".join(head + txt) + "\n")
+    print(open(md).read())
 
 
 def main():
@@ -289,6 +503,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-ceiling", action="store_true")
+    ap.add_argument("--no-oracle-lines", action="store_true",
+                    help="skip the oracle's count of algorithmic bytes (roofline.achieved is null)")
     ap.add_argument("--shared", action="store_true",
                     help="instead of the benchmark: minibatches sharing one candidate set")
     ap.add_argument("--verify", action="store_true",
@@ -313,7 +529,19 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
                          "used to scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
+    ap.add_argument("--summarize", metavar="DIR", default=None,
+                    help="only write the profiles/ summaries of --config from the rocprofv3 output "
+                         "under DIR (see profile_commands)")
+    ap.add_argument("--print-profile-commands", action="store_true",
+                    help="only print the rocprofv3 commands whose output --summarize reads")
     args = ap.parse_args()
+
+    if args.print_profile_commands:
+        print("\n".join(profile_commands(args.config, args.steps)))
+        return
+    if args.summarize:
+        summarize_profiles(args.config, args.summarize, args.steps)
+        return
 
     if args.copy_calibration:
         import torch
@@ -341,7 +569,8 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     torch.cuda.set_device(0)
-    threads = args.threads or min(16, len(os.sched_getaffinity(0)))
+    threads, visible = host_threads()
+    threads = args.threads or threads
     cfg = kgsynth.CONFIGS[args.config]
     types = args.types.split(",") if args.types else list(cfg.query_types)
 
@@ -366,16 +595,24 @@ def main():
         return
     neg_tries = 4 * cfg.n_neg
     dags = {qt: sm.query_preset(qt) for qt in types}
-    argv = {qt: sm.make_args(cfg.batch, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries) for qt in types}
-    outs = {qt: sm.alloc_outputs(cfg.batch, cfg.n_neg) for qt in types}
+    B = cfg.batch
 
-    # untimed accounting pass: graph bytes / 64-byte lines the verification
-    # reads, [0:2] in the candidate kernel, [2:4] in the long-list kernel
+    def step_args(k):
+        # step k samples query ids [k * B, (k + 1) * B): a new batch every step
+        return {qt: sm.make_args(B, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries, query_offset=k * B)
+                for qt in types}
+
+    outs = {qt: sm.alloc_outputs(B, cfg.n_neg) for qt in types}
+
+    # untimed accounting pass on the first batch: graph bytes / 64-byte lines
+    # the verification kernels read by their own tally, [0:2] in the
+    # candidate kernel, [2:4] in the long-list kernel
     acct = {}
+    first = step_args(0)
     for qt in types:
-        stats = torch.zeros((cfg.batch, 4), dtype=torch.int64, device="cuda")
-        sm.sample_positives(g, dags[qt], argv[qt], outs[qt], stream)
-        sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], stats, stream)
+        stats = torch.zeros((B, 4), dtype=torch.int64, device="cuda")
+        sm.sample_positives(g, dags[qt], first[qt], outs[qt], stream)
+        sm.sample_negatives(g, dags[qt], first[qt], outs[qt], stats, stream)
         torch.cuda.synchronize()
         st = stats.sum(0).cpu().numpy()
         nv = outs[qt]["n_valid"].cpu().numpy()
@@ -423,7 +660,9 @@ def main():
                 stream.wait_event(e)
         chain[0] = None
 
-    def split_step(ev):
+    # events per (step, shape): 0/1 positives, 5/2 negative stage, 3/4 the
+    # candidate kernel, 6/7 the long-list kernel (first round)
+    def split_step(ev, argv):
         for qt in types:
             s = streams[qt]
             ev[qt][0].record(s)
@@ -441,13 +680,14 @@ def main():
                                 part=sm.NEG_CANDIDATES, workspace=parts_ws[qt])
             drawn[qt].record(cand_stream)
             s.wait_event(drawn[qt])
+            sm.profile_kernel(ev[qt][6], ev[qt][7], sm.KERNEL_HEAVY)
             sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s, part=sm.NEG_REST,
                                 workspace=parts_ws[qt])
             ev[qt][2].record(s)
 
-    def step(ev):
+    def step(ev, argv):
         if args.split:
-            split_step(ev)
+            split_step(ev, argv)
             return
         for qt in types:   # positives first: they wait for nothing but their own stream
             s = streams[qt]
@@ -463,17 +703,20 @@ def main():
                     s.wait_event(chain[0])
             ev[qt][5].record(s)
             sm.profile_kernel(ev[qt][3], ev[qt][4], sm.KERNEL_CANDIDATES)
+            sm.profile_kernel(ev[qt][6], ev[qt][7], sm.KERNEL_HEAVY)
             sm.sample_negatives(g, dags[qt], argv[qt], outs[qt], None, s)
             ev[qt][2].record(s)
             chain[0] = ev[qt][4]
 
-    warm = {qt: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for qt in types}
+    NEV = 8
+    warm = {qt: [torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for qt in types}
+    all_args = [step_args(k) for k in range(args.warmup + args.steps)]
     fork()
-    for _ in range(args.warmup):
-        step(warm)
+    for k in range(args.warmup):
+        step(warm, all_args[k])
     merge()
     torch.cuda.synchronize()
-    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for qt in types}
+    evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for qt in types}
            for _ in range(args.steps)]
     for e in evs:                       # create the HIP events before the timed region
         for qt in types:
@@ -487,7 +730,7 @@ def main():
     h0 = time.perf_counter()
     fork()
     for k in range(args.steps):
-        step(evs[k])
+        step(evs[k], all_args[args.warmup + k])
     merge()
     t_end.record(stream)
     host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
@@ -497,65 +740,94 @@ def main():
     log(f"host enqueue {host_ms:.3f} ms per step, device {ms_step:.3f} ms per step")
     # the schedule must not change a row: the last timed step's outputs
     # against one plain call per shape on the timing stream
+    last = all_args[-1]
     for qt in types:
-        ref = sm.alloc_outputs(cfg.batch, cfg.n_neg)
-        sm.sample_positives(g, dags[qt], argv[qt], ref, stream)
-        sm.sample_negatives(g, dags[qt], argv[qt], ref, None, stream)
+        ref = sm.alloc_outputs(B, cfg.n_neg)
+        sm.sample_positives(g, dags[qt], last[qt], ref, stream)
+        sm.sample_negatives(g, dags[qt], last[qt], ref, None, stream)
         torch.cuda.synchronize()
         for k, v in ref.items():
             if not torch.equal(v, outs[qt][k]):
                 raise SystemExit(f"bench: {qt} {k} of the timed schedule differs from a plain call")
         del ref
     log("schedule check: every shape's rows equal those of a plain call")
+
+    og = None
+    if not (args.no_cpu_baseline and args.no_oracle_lines):
+        import oracle
+        t0 = time.time()
+        og = oracle.Graph(triples, cfg.n_entities, cfg.n_relations, cfg.add_inverse, threads=threads)
+        log(f"oracle graph built in {time.time() - t0:.1f} s")
+    del triples
+    lines = None if args.no_oracle_lines else oracle_lines(og, cfg, types, neg_tries, threads)
+
     per_type = {}
     for qt in types:
         pos = float(np.mean([e[qt][0].elapsed_time(e[qt][1]) for e in evs]))
         neg = float(np.mean([e[qt][5].elapsed_time(e[qt][2]) for e in evs]))
         cand = float(np.mean([e[qt][3].elapsed_time(e[qt][4]) for e in evs]))
+        heavy = float(np.mean([e[qt][6].elapsed_time(e[qt][7]) for e in evs]))
         a = acct[qt]
         # with --prepare-ahead the negative stage includes the wait for the
         # previous shape's candidate kernel: no per-shape rates then
         rated = not (args.prepare_ahead or args.split or args.concurrent)
         per_type[qt] = {
-            "queries_per_s": cfg.batch / ((pos + neg) / 1e3) if rated else None,
+            "queries_per_s": B / ((pos + neg) / 1e3) if rated else None,
             "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3) if rated else None,
             "positive_ms": pos, "negative_stage_ms": neg, "candidate_kernel_ms": cand,
-            "candidate_kernel_line_GBps": a["cand_lines"] * 64 / (cand / 1e3) / 1e9,
-            "candidate_kernel_useful_GBps": a["cand_bytes"] / (cand / 1e3) / 1e9,
+            "long_list_kernel_ms": heavy,
             "draws_per_query": a["draws"] / max(a["valid"], 1),
-            "cand_line_bytes_per_query": a["cand_lines"] * 64 / max(a["valid"], 1),
-            "cand_useful_bytes_per_query": a["cand_bytes"] / max(a["valid"], 1),
-            "heavy_useful_bytes_per_query": a["heavy_bytes"] / max(a["valid"], 1),
+            "cand_tally_line_bytes_per_query": a["cand_lines"] * 64 / max(a["valid"], 1),
+            "heavy_tally_line_bytes_per_query": a["heavy_lines"] * 64 / max(a["valid"], 1),
             "valid": a["valid"], "complete": a["complete"],
         }
+        if lines:
+            L = lines[qt]
+            per_type[qt]["oracle_first_pass_bytes_per_query"] = L["part0_bytes"] / max(L["queries"], 1)
+            per_type[qt]["oracle_long_list_bytes_per_query"] = L["part1_bytes"] / max(L["queries"], 1)
         log(f"{qt}: {per_type[qt]}")
-    value = cfg.batch * len(types) / (ms_step / 1e3)
+    value = B * len(types) / (ms_step / 1e3)
 
-    # dominant kernel: the candidate kernel (the largest single kernel of the
-    # step) of the shape where it takes longest; timed by events the library
-    # records around it on the sampling stream
-    dom = max(types, key=lambda qt: per_type[qt]["candidate_kernel_ms"])
-    d = per_type[dom]
-    achieved = d["candidate_kernel_line_GBps"]
-    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 5),
-                "traffic": traffic_for(f"k_candidates<{dom}> r0"),
-                "kernel": f"k_candidates<{dom}> (first round of smore_sample_negatives)",
-                "bytes_per_launch": acct[dom]["cand_lines"] * 64,
-                "useful_bytes_per_launch": acct[dom]["cand_bytes"],
-                "avg_launch_ms": round(d["candidate_kernel_ms"], 4),
-                "launch_timing": ("HIP events around the launch on its stream, one stream for the step"
-                                  if args.serial else
-                                  "HIP events around the launch on the candidate stream, where the "
-                                  "shapes' candidate kernels run back to back; positives and the "
-                                  "long-list and selection kernels run beside it on the shapes' streams"
-                                  if args.split else
-                                  "HIP events around the launch on its shape's stream; positives and the "
-                                  "long-list and selection kernels of other shapes may run beside it"),
-                "accounting": "64-byte lines of graph data per dependent read of the candidate "
-                              "kernel (in-edge mask word, reverse node pointers, relation-search "
-                              "probes, group bounds, short backward lists, forward lists staged "
-                              "once per query), times 64, summed over the launch"}
+    timing = ("HIP events around the launch on its stream, one stream for the step" if args.serial else
+              "HIP events around the launch on the candidate stream (candidate kernels back to back); "
+              "other kernels run beside it on the shapes' streams" if args.split else
+              "HIP events around the launch on its shape's stream; kernels of other shapes may run "
+              "beside it")
+
+    def kernel_roofline(qt, kind):
+        d = per_type[qt]
+        ms = d["candidate_kernel_ms"] if kind == "cand" else d["long_list_kernel_ms"]
+        name = f"k_candidates<{qt}> r0" if kind == "cand" else f"k_heavy<{qt}> r0"
+        tally = acct[qt]["cand_lines" if kind == "cand" else "heavy_lines"] * 64
+        algo = None
+        if lines:
+            algo = lines[qt]["part0_bytes" if kind == "cand" else "part1_bytes"]
+        traffic = traffic_for(cfg.name, name)
+        gbps = lambda nbytes: nbytes / (ms / 1e3) / 1e9 if nbytes is not None and ms > 0 else None
+        achieved = gbps(algo)
+        r = {"bound": "hbm", "achieved": None if achieved is None else round(achieved, 2),
+             "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+             "frac": None if achieved is None else round(achieved / HBM_PEAK_GBPS, 5),
+             "traffic": traffic, "kernel": name, "avg_launch_ms": round(ms, 4),
+             "algorithmic_bytes_per_launch": algo,
+             "kernel_tally_bytes_per_launch": tally,
+             "kernel_tally_frac": round(gbps(tally) / HBM_PEAK_GBPS, 5) if ms > 0 else None,
+             "traffic_frac": (round(gbps(traffic) / HBM_PEAK_GBPS, 5) if traffic is not None and ms > 0
+                              else None),
+             "launch_timing": timing}
+        return r
+
+    kernels = [kernel_roofline(qt, kind) for qt in types for kind in ("cand", "heavy")]
+    dom = max(kernels, key=lambda r: r["avg_launch_ms"])
+    roofline = dict(dom)
+    roofline["accounting"] = (
+        "achieved = algorithmic bytes / avg_launch_ms; algorithmic bytes = 64 x the distinct 64-byte "
+        "lines per query that the oracle's bidirectional check under the strict node cut reads for "
+        "the first round's candidate draws (node entries, group search, lists of the device layout), "
+        "summed over the batch; the candidate kernel is charged the first verification pass, the "
+        "long-list kernel the lists longer than 8 entries and forward sets over 1,024 entries; "
+        "kernel_tally is the kernel's own count of the lines of each read it makes; traffic is "
+        "rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by a plain copy")
 
     ceiling = None if args.no_gather_ceiling else gather_ceiling(stream)
     if ceiling:
@@ -563,23 +835,28 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, triples, types, args.cpu_seconds, threads)
+        cpu = cpu_baseline(cfg, og, types, args.cpu_seconds, threads, visible)
+    del og
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": workload_name(cfg, types), "types": types, "batch": cfg.batch,
+        "config": {"workload": workload_name(cfg, types), "types": types, "batch": B,
                    "n_neg": cfg.n_neg, "neg_tries": neg_tries, "pos_tries": 64,
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed,
+                   "query_ids": f"step k samples ids [k x {B}, (k + 1) x {B})",
                    "streams": 1 if args.serial else len(types) + (1 if args.split else 0),
                    "schedule": "serial" if args.serial else "split" if args.split else
                                "concurrent" if args.concurrent else
-                               "chained, prepare ahead" if args.prepare_ahead else "chained"},
+                               "chained, prepare ahead" if args.prepare_ahead else "chained",
+                   "sample_hip_sha256_16": sample_hip_sha()},
         "roofline": roofline,
+        "kernels": kernels,
         "cpu_baseline": cpu,
         "gather_ceiling": ceiling,
+        "oracle_lines": lines,
         "per_type": {qt: {k: (round(v, 4) if isinstance(v, float) else v)
                           for k, v in per_type[qt].items()} for qt in types},
         "graph_build_s": round(build_s, 3),

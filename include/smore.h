@@ -306,10 +306,12 @@ int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_s
    made by this thread records the caller's HIP events (hipEvent_t) on its
    stream immediately before and after one of its kernels in the first
    round of candidate draws: which = 0 the candidate kernel, 1 the kernel
-   that intersects long lists, 2 the ordered selection.  One-shot: the
+   that intersects long lists, 2 the ordered selection.  Each `which` has
+   its own arm, so one call can time several kernels.  One-shot: the
    next smore_sample, smore_sample_negatives or smore_sample_negatives_part
-   call of this thread disarms it whether or not it recorded, also when
-   that call fails validation.  Either event NULL disarms.  The events stay owned by the
+   call of this thread disarms all of them whether or not they recorded,
+   also when that call fails validation.  Either event NULL disarms that
+   `which`.  The events stay owned by the
    caller.  Returns SMORE_E_INVALID_ARG for another `which`. */
 int smore_profile_kernel(void *start_event, void *stop_event, int32_t which);
 

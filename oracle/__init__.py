@@ -78,6 +78,9 @@ def lib():
         L.oracle_answer_set.restype = ctypes.c_int64
         L.oracle_answer_set.argtypes = [P, ctypes.c_int, P, P, P, ctypes.c_int64]
         L.oracle_bidir_check.argtypes = [P, ctypes.c_int, P, P, ctypes.c_uint32, ctypes.c_int32, P]
+        L.oracle_verify_lines_batch.argtypes = [P, ctypes.c_int, ctypes.c_int32, P, P, P,
+                                                 ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64,
+                                                 ctypes.c_int32, P, ctypes.c_int]
         L.oracle_set_proj_mode.argtypes = [ctypes.c_int]
         L.oracle_type_plan.argtypes = [ctypes.c_int, P, P, P, P]
         _lib = L
@@ -212,6 +215,22 @@ class Graph:
         if rc != 0:
             raise ValueError("oracle_verify rejected its arguments")
         return {"mask": mask, "n_valid": nv}
+
+    def verify_lines(self, qtype: str, anchors, relations, positive, cut_mask: int, seed: int,
+                     query_offset: int, n_draws: int, threads: int = 0) -> np.ndarray:
+        """Distinct 64-byte lines a bidirectional check reads per query
+        (oracle_verify_lines_batch): int64 [batch, 3] = first-pass part,
+        long-list part, both."""
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(relations, np.int32)
+        p = np.ascontiguousarray(positive, np.int32)
+        out = np.zeros((len(p), 3), np.int64)
+        rc = lib().oracle_verify_lines_batch(self._h, TYPES.index(qtype), len(p), a.ctypes.data,
+                                             r.ctypes.data, p.ctypes.data, cut_mask, seed,
+                                             query_offset, n_draws, out.ctypes.data, threads)
+        if rc != 0:
+            raise ValueError("oracle_verify_lines rejected its arguments")
+        return out
 
     def sample_shared(self, qtype: str, batch: int, n_shared: int, seed: int = 0,
                       query_offset: int = 0, pos_tries: int = 64, neg_tries: int | None = None,

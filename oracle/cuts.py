@@ -73,3 +73,21 @@ def mask(cut):
     for v in cut:
         m |= 1 << v
     return m
+
+
+def strict(op, child, root):
+    """The optimal cut the DP's top-down construction returns with a strict
+    comparison (appendix on the optimal cut: a node joins the cut only when
+    its children's best cost is larger): among the optimal cuts, the one
+    that caches least far forward, i.e. with the smallest total number of
+    projections between the anchors and their cut node."""
+    best, cand = optimal(op, child, root)
+
+    def forward_depth(cut):
+        total = 0
+        for p in anchor_paths(op, child, root):
+            pos = next(m for m, v in enumerate(p) if v in cut)
+            total += sum(1 for m in range(pos) if op[p[m + 1]] == 1)
+        return total
+
+    return min(cand, key=lambda c: (forward_depth(c), sorted(c)))

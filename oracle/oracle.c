@@ -84,6 +84,8 @@ struct okg {
     int64_t *rs_off;            /* [V+1] first reverse segment of each entity */
     int32_t *rs_rel;            /* [S_rev] */
     int64_t *rs_beg;            /* [S_rev+1] edge range of each reverse segment */
+    int64_t *fs_off;            /* [V+1] first forward segment of each entity */
+    int32_t *fs_rel;            /* [S_fwd] relation of each forward segment */
     int64_t S_fwd, S_rev;
     int32_t *active_in;
     int64_t n_active;
@@ -179,6 +181,7 @@ void oracle_graph_free(okg *g)
     free(g->f_off); free(g->f_rel); free(g->f_nbr);
     free(g->r_off); free(g->r_rel); free(g->r_nbr);
     free(g->rs_off); free(g->rs_rel); free(g->rs_beg);
+    free(g->fs_off); free(g->fs_rel);
     free(g->active_in);
     free(g);
 }
@@ -212,11 +215,23 @@ okg *oracle_graph_build(const int32_t *triples, int64_t n, int32_t V, int32_t R,
     int rc = group_sort(&fc, rev_edge, m, V, nthreads, &g->r_off, &g->r_rel, &g->r_nbr, &m2);
     free(head);
     if (rc || m2 != m) { oracle_graph_free(g); return NULL; }
-    /* forward segment count; reverse segments (runs of one relation) */
+    /* forward segments (runs of one relation per entity) and their relations */
     g->S_fwd = 0;
     for (int32_t v = 0; v < V; v++)
         for (int64_t k = g->f_off[v]; k < g->f_off[v + 1]; k++)
             if (k == g->f_off[v] || g->f_rel[k] != g->f_rel[k - 1]) g->S_fwd++;
+    g->fs_off = (int64_t *)malloc(((size_t)V + 1) * 8);
+    g->fs_rel = (int32_t *)malloc((size_t)(g->S_fwd > 0 ? g->S_fwd : 1) * 4);
+    if (!g->fs_off || !g->fs_rel) { oracle_graph_free(g); return NULL; }
+    {
+        int64_t sf = 0;
+        for (int32_t v = 0; v < V; v++) {
+            g->fs_off[v] = sf;
+            for (int64_t k = g->f_off[v]; k < g->f_off[v + 1]; k++)
+                if (k == g->f_off[v] || g->f_rel[k] != g->f_rel[k - 1]) g->fs_rel[sf++] = g->f_rel[k];
+        }
+        g->fs_off[V] = sf;
+    }
     int64_t S = 0;
     for (int32_t v = 0; v < V; v++)
         for (int64_t k = g->r_off[v]; k < g->r_off[v + 1]; k++)
@@ -686,6 +701,11 @@ static void sample_one(const okg *g, const otype *T, const oracle_args *a, int64
     }
     positive[b] = root;
     for (int k = 0; k < 3; k++) { anchors[3 * b + k] = w.anchors[k]; relations[3 * b + k] = w.relations[k]; }
+    if (a->n_neg == 0) {   /* no candidates: the answer set is not needed */
+        n_valid[b] = 0;
+        neg_draws[b] = 0;
+        return;
+    }
     /* negatives: rejection sampling against the full answer set */
     iset Aq = eval_node(g, T, T->root, w.anchors, w.relations);
     uint32_t cap = 16;
@@ -905,4 +925,233 @@ int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const in
     for (int k = 0; k < T->n; k++) free(B.F[k].v);
     if (counts) { counts[0] = fwd; counts[1] = B.visited; }
     return in;
+}
+
+/* ------------------------------------------------- reads of the method */
+/* Memory lines a bidirectional check reads (Sec. 3.2: the cost discussion
+   and the optimal-scheduling equation count the entities each side
+   expands; this counts the 64-byte lines of graph data behind them, the
+   unit the memory system moves).  The adjacency is laid out per direction
+   as node[V+1] (int32: an entity's first group), grp[S+1] (int32 pairs:
+   relation, first edge) and nbr[E] (int32), each array starting on a
+   64-byte boundary; a line is a 64-byte block of one array.  Group and edge
+   indices are those of the canonical order (entity, relation, neighbour
+   ascending), which this oracle's arrays share with any CSR of the same
+   graph.  Reads:
+   - an entity's groups: the node entries v and v + 1;
+   - the group of relation r: a lower-bound binary search over the entity's
+     groups (probe (lo + hi) / 2, compare its relation), then the edge
+     bounds of the group found (its entry and the next one);
+   - a neighbour list that is expanded: its entries in ascending order, up
+     to the first one that decides the check;
+   - a list met with a forward-cached set: the shorter side gives the keys
+     in ascending order (list keys are read, cached keys are free), each
+     key is looked up in the other side by the same lower-bound search
+     (probes of a list are read, of a cached set free), up to the first
+     common entity;
+   - forward caching: every cut set once, from the anchors, with the same
+     reads (node entries, group search, the whole list).
+   The candidates of query qid are draws j < n_draws, c_j =
+   pick(U(NEG, qid, 0, j), V).  Lines fall in two parts: part 0 holds the
+   forward caching, each candidate's own node entries and group search,
+   edge tests against an anchor, and the expansion of backward lists of at
+   most LONG_LIST entries when every forward-cached set of the query fits
+   the STAGE_BUDGET entries staged per query; part 1 holds everything read
+   below a longer list or with a set that does not fit.  Each part counts
+   its distinct lines; the total counts distinct lines over both. */
+#define LONG_LIST 8
+#define STAGE_BUDGET 1024
+enum { L_FNODE = 0, L_FGRP, L_FNBR, L_RNODE, L_RGRP, L_RNBR };
+
+typedef struct { int64_t *v; int64_t n, cap; } lineset;
+
+static void ls_add(lineset *s, int arr, int64_t byte_off, int64_t nbytes)
+{
+    for (int64_t l = byte_off >> 6; l <= (byte_off + nbytes - 1) >> 6; l++) {
+        if (s->n == s->cap) {
+            s->cap = s->cap ? 2 * s->cap : 256;
+            s->v = (int64_t *)realloc(s->v, (size_t)s->cap * 8);
+        }
+        s->v[s->n++] = ((int64_t)arr << 56) | l;
+    }
+}
+
+static int cmp_i64(const void *a, const void *b)
+{
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    return x < y ? -1 : x > y;
+}
+
+static int64_t ls_distinct(int64_t *v, int64_t n)
+{
+    if (n == 0) return 0;
+    qsort(v, (size_t)n, 8, cmp_i64);
+    int64_t d = 1;
+    for (int64_t i = 1; i < n; i++) d += v[i] != v[i - 1];
+    return d;
+}
+
+typedef struct {
+    const okg *g;
+    const otype *T;
+    uint32_t cut;
+    iset F[8];
+    int all_staged;
+    const int32_t *anchors, *relations;
+    lineset part[2];
+} vlines;
+
+/* the group of relation r of entity v in one direction: [*b, *e), or 0 */
+static int vgroup(vlines *L, int part, int dir, int32_t v, int32_t r, int64_t *b, int64_t *e)
+{
+    const okg *g = L->g;
+    const int64_t *soff = dir ? g->rs_off : g->fs_off;
+    const int32_t *srel = dir ? g->rs_rel : g->fs_rel;
+    const int arr = dir ? L_RGRP : L_FGRP;
+    ls_add(&L->part[part], dir ? L_RNODE : L_FNODE, (int64_t)v * 4, 8);
+    int64_t lo = soff[v], hi = soff[v + 1];
+    const int64_t end = hi;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        ls_add(&L->part[part], arr, mid * 8, 4);
+        if (srel[mid] < r) lo = mid + 1; else hi = mid;
+    }
+    if (lo == end || srel[lo] != r) return 0;
+    ls_add(&L->part[part], arr, lo * 8 + 4, 4);
+    ls_add(&L->part[part], arr, (lo + 1) * 8 + 4, 4);
+    rel_range(dir ? g->r_off : g->f_off, dir ? g->r_rel : g->f_rel, v, r, b, e);
+    return 1;
+}
+
+/* does the reverse list [b, e) share an entity with the cached set F? */
+static int vmeet(vlines *L, int part, int64_t b, int64_t e, iset F)
+{
+    const int32_t *nbr = L->g->r_nbr;
+    if (e - b <= F.n) {
+        for (int64_t i = b; i < e; i++) {
+            ls_add(&L->part[part], L_RNBR, i * 4, 4);
+            if (set_has(F, nbr[i])) return 1;
+        }
+        return 0;
+    }
+    for (int64_t k = 0; k < F.n; k++) {
+        int64_t lo = b, hi = e;
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            ls_add(&L->part[part], L_RNBR, mid * 4, 4);
+            if (nbr[mid] < F.v[k]) lo = mid + 1; else hi = mid;
+        }
+        if (lo < e) {
+            ls_add(&L->part[part], L_RNBR, lo * 4, 4);
+            if (nbr[lo] == F.v[k]) return 1;
+        }
+    }
+    return 0;
+}
+
+static int vmember(vlines *L, int k, int32_t x, int part)
+{
+    if (L->cut & (1u << k)) return set_has(L->F[k], x);
+    const onode *nd = &L->T->nd[k];
+    if (nd->op == N_ANCHOR) return x == L->anchors[nd->slot];
+    if (nd->op == N_NOT) return !vmember(L, nd->ch[0], x, part);
+    if (nd->op == N_AND || nd->op == N_OR) {
+        for (int c = 0; c < nd->nch; c++) {
+            const int in = vmember(L, nd->ch[c], x, part);
+            if (nd->op == N_AND && !in) return 0;
+            if (nd->op == N_OR && in) return 1;
+        }
+        return nd->op == N_AND;
+    }
+    /* projection: x is in A_r(S) iff some y with (y, r, x) in E lies in S */
+    int64_t b, e;
+    if (!vgroup(L, part, 1, x, L->relations[nd->slot], &b, &e)) return 0;
+    const int ch = nd->ch[0];
+    const int edge_test = (L->cut & (1u << ch)) && L->T->nd[ch].op == N_ANCHOR;
+    const int p = edge_test ? part : (e - b > LONG_LIST || !L->all_staged) ? 1 : part;
+    if (L->cut & (1u << ch)) return vmeet(L, p, b, e, L->F[ch]);
+    for (int64_t i = b; i < e; i++) {
+        ls_add(&L->part[p], L_RNBR, i * 4, 4);
+        if (vmember(L, ch, L->g->r_nbr[i], p)) return 1;
+    }
+    return 0;
+}
+
+/* reads of forward caching: the set at node k computed from the anchors */
+static void vforward(vlines *L, int k)
+{
+    const onode *nd = &L->T->nd[k];
+    if (nd->op == N_ANCHOR) return;
+    for (int c = 0; c < nd->nch; c++) vforward(L, nd->ch[c]);
+    if (nd->op != N_PROJ) return;
+    iset S = eval_node(L->g, L->T, nd->ch[0], L->anchors, L->relations);
+    for (int64_t i = 0; i < S.n; i++) {
+        int64_t b, e;
+        if (vgroup(L, 0, 0, S.v[i], L->relations[nd->slot], &b, &e) && e > b)
+            ls_add(&L->part[0], L_FNBR, b * 4, (e - b) * 4);
+    }
+    free(S.v);
+}
+
+int oracle_verify_lines(const okg *g, int qtype, const int32_t *anchors, const int32_t *relations,
+                        uint32_t cut_mask, uint64_t seed, uint32_t qid, int32_t n_draws,
+                        int64_t *lines)
+{
+    if (!g || qtype < 0 || qtype >= NTYPES || n_draws < 0) return -1;
+    const otype *T = &TYPES[qtype];
+    if (!is_node_cut(T, cut_mask)) return -1;
+    for (int k = 0; k < T->n; k++) {
+        const onode *nd = &T->nd[k];
+        if (nd->op == N_ANCHOR && (anchors[nd->slot] < 0 || anchors[nd->slot] >= g->V)) return -1;
+        if (nd->op == N_PROJ && (relations[nd->slot] < 0 || relations[nd->slot] >= g->R)) return -1;
+    }
+    vlines L;
+    memset(&L, 0, sizeof(L));
+    L.g = g; L.T = T; L.cut = cut_mask; L.anchors = anchors; L.relations = relations;
+    int64_t staged = 0;
+    L.all_staged = 1;
+    for (int k = 0; k < T->n; k++)
+        if (cut_mask & (1u << k)) {
+            L.F[k] = eval_node(g, T, k, anchors, relations);
+            vforward(&L, k);
+            if (T->nd[k].op != N_ANCHOR) {
+                staged += L.F[k].n;
+                if (staged > STAGE_BUDGET) L.all_staged = 0;
+            }
+        }
+    for (int32_t j = 0; j < n_draws; j++) {
+        const int32_t c = (int32_t)oracle_pick(oracle_draw(seed, TAG_NEG, qid, 0, (uint32_t)j),
+                                               (uint64_t)g->V);
+        (void)vmember(&L, T->root, c, 0);
+    }
+    int64_t *all = (int64_t *)malloc((size_t)(L.part[0].n + L.part[1].n + 1) * 8);
+    memcpy(all, L.part[0].v, (size_t)L.part[0].n * 8);
+    memcpy(all + L.part[0].n, L.part[1].v, (size_t)L.part[1].n * 8);
+    lines[0] = ls_distinct(L.part[0].v, L.part[0].n);
+    lines[1] = ls_distinct(L.part[1].v, L.part[1].n);
+    lines[2] = ls_distinct(all, L.part[0].n + L.part[1].n);
+    free(all);
+    free(L.part[0].v);
+    free(L.part[1].v);
+    for (int k = 0; k < T->n; k++) free(L.F[k].v);
+    return 0;
+}
+
+int oracle_verify_lines_batch(const okg *g, int qtype, int32_t batch, const int32_t *anchors,
+                              const int32_t *relations, const int32_t *positive, uint32_t cut_mask,
+                              uint64_t seed, uint64_t query_offset, int32_t n_draws, int64_t *lines,
+                              int nthreads)
+{
+    if (!g || qtype < 0 || qtype >= NTYPES || batch < 0) return -1;
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads) reduction(| : bad)
+    for (int64_t b = 0; b < batch; b++) {
+        int64_t *out = lines + 3 * b;
+        out[0] = out[1] = out[2] = 0;
+        if (positive[b] < 0) continue;   /* no query: nothing is verified */
+        bad |= oracle_verify_lines(g, qtype, anchors + 3 * b, relations + 3 * b, cut_mask, seed,
+                                   (uint32_t)(query_offset + (uint64_t)b), n_draws, out) != 0;
+    }
+    return bad ? -1 : 0;
 }

@@ -106,6 +106,32 @@ int64_t oracle_answer_set(const okg *g, int qtype, const int32_t *anchors,
 int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const int32_t *relations,
                        uint32_t cut_mask, int32_t c, int64_t *counts);
 
+/* Memory lines a bidirectional check of one query reads (Sec. 3.2, the
+   cost of forward caching plus backward verification), on the device
+   layout node[V+1] / grp[S+1] pairs / nbr[E] per direction with 64-byte
+   lines: forward caching of every set of the node cut cut_mask, then for
+   each candidate draw j < n_draws (pick(U(NEG, qid, 0, j), V)) the
+   backward check from the candidate.  The rules of each read are stated
+   with the definition in oracle.c.  lines[0]: distinct lines of the part
+   a first verification pass makes (forward caching, each candidate's
+   entity range and group search, edge tests against anchors, backward
+   lists of at most 8 entries when the query's cached sets fit 1,024
+   staged entries); lines[1]: distinct lines read below a longer list or
+   with a set that does not fit; lines[2]: distinct lines of both.
+   Returns 0, or -1 for a bad shape, ids out of range or a mask that is
+   not a node cut. */
+int oracle_verify_lines(const okg *g, int qtype, const int32_t *anchors, const int32_t *relations,
+                        uint32_t cut_mask, uint64_t seed, uint32_t qid, int32_t n_draws,
+                        int64_t *lines);
+
+/* oracle_verify_lines for queries b < batch (anchors / relations [batch*3],
+   positive [batch]: a row with positive < 0 has no query and gets zeros),
+   query ids query_offset + b; lines [batch*3]. */
+int oracle_verify_lines_batch(const okg *g, int qtype, int32_t batch, const int32_t *anchors,
+                              const int32_t *relations, const int32_t *positive, uint32_t cut_mask,
+                              uint64_t seed, uint64_t query_offset, int32_t n_draws, int64_t *lines,
+                              int nthreads);
+
 /* Projection set-building mode, for tests: 0 auto, 1 always sort-unique,
    2 always a bitmap over V.  Results are identical in every mode. */
 void oracle_set_proj_mode(int mode);

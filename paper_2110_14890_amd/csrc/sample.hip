@@ -1557,11 +1557,12 @@ inline int check_launch(const char** err)
     return SMORE_OK;
 }
 
+// One-shot event pairs of the next negatives call, one per kernel kind
+// (0 candidate kernel, 1 long-list kernel, 2 selection), each independent.
 struct ProfileArm {
     hipEvent_t start = nullptr, stop = nullptr;
-    int which = -1;
 };
-thread_local ProfileArm g_prof;
+thread_local ProfileArm g_prof[3];
 
 // One-shot wait of the next negatives call: its stream waits on this event
 // right before the first candidate kernel, after the preparation.
@@ -1569,9 +1570,10 @@ thread_local hipEvent_t g_wait = nullptr;
 
 inline void prof_mark(int which, int round, bool after, hipStream_t st)
 {
-    if (round != 0 || g_prof.which != which || !g_prof.start || !g_prof.stop) return;
-    (void)hipEventRecord(after ? g_prof.stop : g_prof.start, st);
-    if (after) g_prof = ProfileArm{};
+    ProfileArm& a = g_prof[which];
+    if (round != 0 || !a.start || !a.stop) return;
+    (void)hipEventRecord(after ? a.stop : a.start, st);
+    if (after) a = ProfileArm{};
 }
 
 // parts: NEG_PREPARE the per-query preparation, NEG_CANDIDATES the first
@@ -1874,15 +1876,15 @@ void arm_wait(void* event) { g_wait = (hipEvent_t)event; }
 
 void disarm()
 {
-    g_prof = ProfileArm{};
+    for (ProfileArm& a : g_prof) a = ProfileArm{};
     g_wait = nullptr;
 }
 
 void arm_profile(void* start_event, void* stop_event, int which)
 {
-    g_prof.start = (hipEvent_t)start_event;
-    g_prof.stop = (hipEvent_t)stop_event;
-    g_prof.which = (start_event && stop_event) ? which : -1;
+    ProfileArm& a = g_prof[which];
+    a.start = (start_event && stop_event) ? (hipEvent_t)start_event : nullptr;
+    a.stop = (start_event && stop_event) ? (hipEvent_t)stop_event : nullptr;
 }
 
 size_t negatives_workspace_bytes(const SampleParams& p)

@@ -281,19 +281,25 @@ def test_negation_parity_full_batch(name):
         assert (got["n_valid"] >= 0).mean() > 0.5
 
 
-@pytest.mark.parametrize("name", ["wikikg2"])
-def test_sample_parity_large_sampled_rows(name):
-    # full batch on the GPU in the benchmark's launch configuration; the
-    # oracle recomputes a random subset of rows one query at a time
-    cfg, tr = config_graph(name)
+@pytest.mark.timeout(900)
+def test_sample_parity_wikikg2_full_batch():
+    """The ogbl-wikikg2-shaped graph (2.5M entities, 17M triples; it stands
+    in for that dataset of the KG statistics table, Sec. 5.1): the whole
+    batch of 8,192 queries x 256 negatives of all fourteen shapes, every row
+    against the oracle (run on the host's threads, OMP_NUM_THREADS)."""
+    import time
+
+    cfg, tr = config_graph("wikikg2")
     g, og = graph_pair(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse)
-    rng = np.random.default_rng(0)
+    del tr
     for qt in cfg.query_types + NEG_TYPES:
-        progress(f"{name} {qt}")
         got = gpu_sample(g, qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
-        rows = np.sort(rng.choice(cfg.batch, 96, replace=False))
-        ref = oracle_rows(og, qt, rows, cfg.n_neg, cfg.seed, 4 * cfg.n_neg)
-        assert_same(got, ref, rows=rows, what=f"{name}/{qt}")
+        t = time.time()
+        ref = og.sample(qt, cfg.batch, cfg.n_neg, seed=cfg.seed)
+        progress(f"wikikg2 {qt}: {cfg.batch} rows, oracle {time.time() - t:.1f} s")
+        assert_same(got, ref, what=f"wikikg2/{qt}")
+        assert (got["n_valid"] >= 0).mean() > 0.5
+    g.close()
 
 
 @pytest.mark.parametrize("qt", sm.TYPES)

@@ -1,0 +1,136 @@
+"""Pins of the oracle's count of memory lines a bidirectional check reads
+(oracle_verify_lines; the cost of forward caching and backward verification,
+Sec. 3.2, in 64-byte lines of the device layout: node[V+1] int32,
+grp[S+1] int32 pairs, nbr[E] int32 per direction).
+
+* Hand graphs whose group and edge indices are written out here: the lines
+  of every read follow from those indices and the byte offsets 4v, 8s and
+  4e, so each expected line set is derived without the oracle's code.
+* Invariants on random graphs for all fourteen shapes: every draw reads its
+  own node entries (a lower bound from the draws alone), the parts bound
+  the total, a graph whose lists never exceed eight entries puts nothing in
+  the long-list part, and more draws never read fewer lines.
+* The oracle's strict cut (oracle/cuts.py) equals the library planner's."""
+import numpy as np
+import pytest
+
+import kgsynth
+from oracle import cuts as C
+
+TAG_NEG = 2
+
+
+def draws(oracle_lib, seed, qid, n, V):
+    return [oracle_lib.pick(oracle_lib.draw(seed, TAG_NEG, qid, 0, j), V) for j in range(n)]
+
+
+def lines_of(byte_off, nbytes):
+    return set(range(byte_off >> 6, ((byte_off + nbytes - 1) >> 6) + 1))
+
+
+def strict_mask(oracle_lib, qt):
+    op, ch, slot, root = oracle_lib.type_plan(qt)
+    return C.mask(C.strict(op, ch, root))
+
+
+def test_edge_tests_against_an_anchor(oracle_lib):
+    # 1p over anchor 0: edges (0, 0, t) for t = 10 .. 17.  Reverse groups:
+    # entity t -> group t - 10 (one group each); reverse edges: tail t ->
+    # edge t - 10.  The cut is the anchor: nothing is cached forward; a
+    # candidate reads its node entries, and one with an in-edge its group
+    # (search probe and bounds) and its one-entry list.  Group 7 ends on the
+    # next line (its end bound is entry 8, bytes 68..71).
+    V = 200
+    tr = np.array([[0, 0, t] for t in range(10, 18)], np.int32)
+    g = oracle_lib.Graph(tr, V, 1)
+    anchors, rels, pos = np.array([[0, -1, -1]], np.int32), np.array([[0, -1, -1]], np.int32), \
+        np.array([10], np.int32)
+    n, seed = 60, 5
+    hit_seen = crossing_seen = False
+    for qid in range(40):
+        cs = draws(oracle_lib, seed, qid, n, V)
+        node, grp, nbr = set(), set(), set()
+        for c in cs:
+            node |= lines_of(4 * c, 8)
+            if 10 <= c <= 17:
+                s = c - 10
+                crossing_seen |= s == 7
+                grp |= lines_of(8 * s, 4) | lines_of(8 * s + 4, 4) | lines_of(8 * (s + 1) + 4, 4)
+                nbr |= lines_of(4 * s, 4)
+                hit_seen = True
+        got = g.verify_lines("1p", anchors, rels, pos, strict_mask(oracle_lib, "1p"), seed, qid, n)
+        want = len(node) + len(grp) + len(nbr)
+        assert got[0].tolist() == [want, 0, want], qid
+    assert hit_seen and crossing_seen
+
+
+def test_two_hop_long_list_goes_to_the_long_part(oracle_lib):
+    # 2p: anchor 0 -(r0)-> 1..20, each of 1..20 -(r1)-> 100; the strict cut
+    # caches F0 = {1..20} (forward group 0 of entity 0, forward edges 0..19).
+    # Reverse groups: entities 1..20 -> groups 0..19 (relation 0), entity 100
+    # -> group 20 (relation 1); reverse edges: tails 1..20 -> edges 0..19,
+    # tail 100 -> edges 20..39 (heads 1..20).  R_r1(100) has 20 > 8 entries:
+    # it is met with F0 (20 entries, not fewer than the list) by reading the
+    # list in order, and its first entry (entity 1, edge 20) is in F0.
+    V = 300
+    tr = [[0, 0, y] for y in range(1, 21)] + [[y, 1, 100] for y in range(1, 21)]
+    g = oracle_lib.Graph(np.array(tr, np.int32), V, 2)
+    anchors, rels = np.array([[0, -1, -1]], np.int32), np.array([[0, 1, -1]], np.int32)
+    pos = np.array([100], np.int32)
+    fwd = lines_of(0, 8) | set()                    # forward node entries of 0
+    fgrp = lines_of(0, 4) | lines_of(4, 4) | lines_of(12, 4)
+    fnbr = lines_of(0, 80)
+    n, seed = 400, 9
+    for qid in (0, 1, 2, 3):
+        cs = draws(oracle_lib, seed, qid, n, V)
+        node, grp, nbr_long = set(), set(), set()
+        for c in cs:
+            node |= lines_of(4 * c, 8)
+            if 1 <= c <= 20:     # in-edges, but none under r1: the search fails
+                grp |= lines_of(8 * (c - 1), 4)
+            elif c == 100:
+                grp |= lines_of(8 * 20, 4) | lines_of(8 * 20 + 4, 4) | lines_of(8 * 21 + 4, 4)
+                nbr_long |= lines_of(4 * 20, 4)
+        got = g.verify_lines("2p", anchors, rels, pos, strict_mask(oracle_lib, "2p"), seed, qid, n)
+        part0 = len(fwd) + len(fgrp) + len(fnbr) + len(node) + len(grp)
+        assert got[0].tolist() == [part0, len(nbr_long), part0 + len(nbr_long)], qid
+        assert (100 in cs) == (len(nbr_long) == 1)
+
+
+@pytest.mark.parametrize("qt", ["1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up",
+                                "2in", "3in", "inp", "pin", "pni"])
+def test_invariants_on_random_graphs(oracle_lib, qt):
+    rng = np.random.default_rng(8)
+    V = 1500
+    tr = kgsynth.random_tiny(rng, V, 4, 9000)
+    g = oracle_lib.Graph(tr, V, 4, add_inverse=True)
+    q = g.sample(qt, 48, 0, seed=2)
+    ok = q["positive"] >= 0
+    assert ok.sum() > 20
+    m = strict_mask(oracle_lib, qt)
+    L40 = g.verify_lines(qt, q["anchors"], q["relations"], q["positive"], m, 2, 0, 40)
+    L80 = g.verify_lines(qt, q["anchors"], q["relations"], q["positive"], m, 2, 0, 80)
+    assert (L40[~ok] == 0).all()
+    for b in np.nonzero(ok)[0]:
+        p0, p1, tot = L40[b]
+        assert max(p0, p1) <= tot <= p0 + p1
+        lower = set()
+        for c in draws(oracle_lib, 2, int(b), 40, V):
+            lower |= lines_of(4 * c, 8)
+        assert p0 >= len(lower)
+        assert (L80[b] >= L40[b]).all()
+    # lists of this graph: reverse groups up to how many entries?
+    e, r, o = g.dump(reverse=True)
+    _, counts = np.unique(e.astype(np.int64) * 64 + r, return_counts=True)
+    if counts.max() <= 8:
+        assert (L40[:, 1] == 0).all()
+
+
+def test_strict_cut_equals_the_library_planner(oracle_lib):
+    sm = pytest.importorskip("paper_2110_14890_amd")
+    import os
+    if not os.path.exists(sm.LIB_PATH):
+        pytest.skip("library not built")
+    for qt in oracle_lib.TYPES:
+        op, ch, slot, root = oracle_lib.type_plan(qt)
+        assert sorted(C.strict(op, ch, root)) == sorted(sm.plan(qt, 0)), qt
