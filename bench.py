@@ -525,6 +525,9 @@ def main():
     ap.add_argument("--prepare-ahead", action="store_true",
                     help="with one stream per shape, let a shape's preparation run before the "
                          "wait for the previous candidate kernel (smore_wait_before_kernel)")
+    ap.add_argument("--pipeline", type=int, default=3,
+                    help="sets of streams and outputs per shape that consecutive steps alternate "
+                         "between (1: one stream per shape)")
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (five times) and exit; "
@@ -602,7 +605,12 @@ def main():
         return {qt: sm.make_args(B, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries, query_offset=k * B)
                 for qt in types}
 
-    outs = {qt: sm.alloc_outputs(B, cfg.n_neg) for qt in types}
+    # steps alternate between `pipeline` sets of streams and outputs per shape
+    # (a workspace per stream), so a step's work on a shape does not queue
+    # behind the previous step's long-list and selection kernels of that shape
+    P = 1 if args.serial or args.split else max(1, args.pipeline)
+    outs_p = [{qt: sm.alloc_outputs(B, cfg.n_neg) for qt in types} for _ in range(P)]
+    outs = outs_p[0]
 
     # untimed accounting pass on the first batch: graph bytes / 64-byte lines
     # the verification kernels read by their own tally, [0:2] in the
@@ -636,9 +644,12 @@ def main():
     # first-round candidate kernel runs on one candidate stream, in chain
     # order, after its preparation on the shape's stream (an event), and the
     # shape's stream takes up the rest of its negatives after it (an event).
-    streams = {qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
+    streams_p = [{qt: (stream if args.serial else torch.cuda.Stream()) for qt in types}
+                 for _ in range(P)]
+    streams = streams_p[0]
     cand_stream = torch.cuda.Stream() if args.split else None
-    all_streams = list(streams.values()) + ([cand_stream] if cand_stream is not None else [])
+    all_streams = ([x for sp in streams_p for x in sp.values()] +
+                   ([cand_stream] if cand_stream is not None else []))
     join = {qt: torch.cuda.Event() for qt in types}
     chain = [None]   # end event of the last candidate kernel launched
     parts_ws = {qt: sm.Workspace() for qt in types}
@@ -685,10 +696,11 @@ def main():
                                 workspace=parts_ws[qt])
             ev[qt][2].record(s)
 
-    def step(ev, argv):
+    def step(ev, argv, k):
         if args.split:
             split_step(ev, argv)
             return
+        streams, outs = streams_p[k % P], outs_p[k % P]
         for qt in types:   # positives first: they wait for nothing but their own stream
             s = streams[qt]
             ev[qt][0].record(s)
@@ -713,7 +725,7 @@ def main():
     all_args = [step_args(k) for k in range(args.warmup + args.steps)]
     fork()
     for k in range(args.warmup):
-        step(warm, all_args[k])
+        step(warm, all_args[k], k)
     merge()
     torch.cuda.synchronize()
     evs = [{qt: [torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for qt in types}
@@ -730,7 +742,7 @@ def main():
     h0 = time.perf_counter()
     fork()
     for k in range(args.steps):
-        step(evs[k], all_args[args.warmup + k])
+        step(evs[k], all_args[args.warmup + k], args.warmup + k)
     merge()
     t_end.record(stream)
     host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
@@ -741,6 +753,7 @@ def main():
     # the schedule must not change a row: the last timed step's outputs
     # against one plain call per shape on the timing stream
     last = all_args[-1]
+    outs = outs_p[(args.warmup + args.steps - 1) % P]
     for qt in types:
         ref = sm.alloc_outputs(B, cfg.n_neg)
         sm.sample_positives(g, dags[qt], last[qt], ref, stream)
@@ -847,10 +860,11 @@ def main():
                    "n_neg": cfg.n_neg, "neg_tries": neg_tries, "pos_tries": 64,
                    "seed": cfg.seed, "graph_seed": cfg.graph_seed,
                    "query_ids": f"step k samples ids [k x {B}, (k + 1) x {B})",
-                   "streams": 1 if args.serial else len(types) + (1 if args.split else 0),
-                   "schedule": "serial" if args.serial else "split" if args.split else
-                               "concurrent" if args.concurrent else
-                               "chained, prepare ahead" if args.prepare_ahead else "chained",
+                   "streams": 1 if args.serial else P * len(types) + (1 if args.split else 0),
+                   "schedule": ("serial" if args.serial else "split" if args.split else
+                                "concurrent" if args.concurrent else
+                                "chained, prepare ahead" if args.prepare_ahead else "chained")
+                               + (f", steps alternate over {P} stream sets" if P > 1 else ""),
                    "sample_hip_sha256_16": sample_hip_sha()},
         "roofline": roofline,
         "kernels": kernels,

@@ -1330,6 +1330,157 @@ __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p,
     }
 }
 
+// Highest lane whose exclusive prefix excl is <= idx (binary lifting over
+// the wavefront; every lane must be active).  excl is nondecreasing over
+// the lanes and 0 in lane 0.
+__device__ __forceinline__ int owner_lane(int32_t idx, int32_t excl)
+{
+    int lo = 0;
+#pragma unroll
+    for (int step = 32; step >= 1; step >>= 1) {
+        const int cand = lo + step;
+        const int32_t ev = __shfl(excl, cand > 63 ? 63 : cand);
+        if (cand <= 63 && ev <= idx) lo = cand;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int32_t excl_prefix(int32_t v, int lane, int32_t* total)
+{
+    int32_t incl = v;
+    for (int d = 1; d < 64; d <<= 1) {
+        const int32_t t = __shfl_up(incl, d);
+        if (lane >= d) incl += t;
+    }
+    *total = uni(__shfl(incl, 63));
+    return incl - v;
+}
+
+// OR of a 64-bit value over the wavefront.
+__device__ __forceinline__ uint64_t wave_or(uint64_t x)
+{
+    for (int s = 32; s > 0; s >>= 1)
+        x |= (uint64_t)(uint32_t)__shfl_xor((int32_t)(uint32_t)x, s) |
+             ((uint64_t)(uint32_t)__shfl_xor((int32_t)(x >> 32), s) << 32);
+    return x;
+}
+
+// The long-list kernel of 3p, batched: wavefront w takes items w,
+// w + nwaves, ... like k_heavy, but decides up to 64 of them together, one
+// per lane.  The entities y of all their candidates' lists R_r2(c) are
+// expanded 64 at a time (signature class, then the group under r1), and
+// the (y, key) pairs of all of them, keys from the shorter of R_r1(y) and
+// the item's F0 = A_r0(a0), are searched 256 at a time; a hit makes its
+// item an answer, and an item's remaining y's are skipped once it is one.
+// A wavefront holds a few items (the queue over the persistent grid), so
+// their dependent chains overlap instead of running one item after the
+// other.  With the read tally, a batch's reads are charged to the query of
+// its first item (the sums over all queries are exact).
+template <class T>
+__global__ __launch_bounds__(HEAVY_WG) void k_heavy3(GraphView g, SampleParams p, smore_sample_out out,
+                                                     Ws ws, int64_t* stats, int nxt)
+{
+    const int lane = threadIdx.x & 63;
+    if (blockIdx.x == 0 && threadIdx.x == 0) ws.ctrl[2 + nxt] = 0;
+    const int32_t total = uni(ws.ctrl[0]);
+    const int32_t nwaves = gridDim.x * (HEAVY_WG / 64);
+    const int32_t w0 = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6));
+    T tl;
+    for (int64_t base = w0; base < total; base += 64 * (int64_t)nwaves) {
+        // this lane's item: candidate list S = R_r2(c), relation r1, F0
+        const int64_t mine = base + (int64_t)lane * nwaves;
+        int32_t b = -1, r1 = 0, f0b = 0, f0n = 0;
+        int64_t mat = 0;
+        int2 S = make_int2(0, 0);
+        if (mine < total) {
+            const int2 it = ws.queue[mine];
+            b = it.x;
+            mat = (int64_t)it.x * p.neg_tries + it.y;
+            const int32_t c = ws.cval[mat];
+            r1 = out.relations[3 * (int64_t)b + 1];
+            const int32_t r2 = out.relations[3 * (int64_t)b + 2];
+            const int32_t* qb = ws.qf + (int64_t)b * QF;
+            f0b = qb[0];
+            f0n = qb[1] - f0b;
+            S = group_range(g.rev, c, r2, tl);
+        }
+        uint64_t ans = 0;     // bit i: the item of lane i is an answer
+        int32_t ydone = 0;    // y's of this lane's item expanded so far
+        // the y's of the items not yet answers, 64 at a time, laid out again
+        // after every chunk
+        for (;;) {
+            const int32_t yrem = ((ans >> lane) & 1) ? 0 : (S.y - S.x) - ydone;
+            int32_t ytotal;
+            const int32_t yex = excl_prefix(yrem, lane, &ytotal);
+            if (ytotal == 0) break;
+            const int it = owner_lane(min(lane, ytotal - 1), yex);
+            const int32_t ipos = __shfl(ydone, it) + lane - __shfl(yex, it);   // y index in its item
+            const int32_t iSx = __shfl(S.x, it), ir1 = __shfl(r1, it);
+            const int32_t if0b = __shfl(f0b, it), if0n = __shfl(f0n, it);
+            int2 s2 = make_int2(0, 0);
+            if (lane < ytotal) {
+                // y without an in-edge under r1's signature class has none under r1
+                const int32_t y = g.rev.nbr[iSx + ipos];
+                tl.read(g.rev.nbr + iSx + ipos, 4);
+                tl.read(g.sig + y, 1);
+                if (g.sig[y] & sig_bit(ir1)) s2 = group_range(g.rev, y, ir1, tl);
+            }
+            const int32_t len = s2.y - s2.x;
+            const bool kil = len <= if0n;            // search R_r1(y)'s entries in F0
+            const int32_t npair = len > 0 ? min(len, if0n) : 0;
+            // pairs 256 at a time over the y's whose item is not yet an
+            // answer: after each step the remaining pairs are laid out again
+            int32_t pdone = 0;                        // this y's pairs searched so far
+            for (;;) {
+                const int32_t rem = ((ans >> it) & 1) ? 0 : npair - pdone;
+                int32_t ptotal;
+                const int32_t pex = excl_prefix(rem, lane, &ptotal);
+                if (ptotal == 0) break;
+                const int32_t* Bk[4];
+                int32_t nbk[4], x[4], who[4];
+                bool cnt[4], found[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int32_t pi = 64 * u + lane;
+                    const int32_t pq = pi < ptotal ? pi : ptotal - 1;
+                    const int yl = owner_lane(pq, pex);
+                    const int32_t off = __shfl(pdone, yl) + pq - __shfl(pex, yl);
+                    const int32_t lx = __shfl(s2.x, yl), ln = __shfl(len, yl);
+                    const int32_t k_in_l = __shfl((int32_t)kil, yl);
+                    const int32_t fb = __shfl(if0b, yl), fn = __shfl(if0n, yl);
+                    who[u] = __shfl(it, yl);
+                    Bk[u] = g.fwd.nbr + fb;
+                    nbk[u] = 0;
+                    x[u] = -1;
+                    cnt[u] = false;
+                    if (pi < ptotal) {
+                        if (k_in_l) {
+                            x[u] = g.rev.nbr[lx + off];
+                            tl.read(g.rev.nbr + lx + off, 4);
+                            nbk[u] = fn;
+                        } else {
+                            x[u] = g.fwd.nbr[fb + off];
+                            Bk[u] = g.rev.nbr + lx;
+                            nbk[u] = ln;
+                            cnt[u] = true;
+                        }
+                    }
+                }
+                search4v(Bk, nbk, x, cnt, found, tl);
+                uint64_t m = 0;
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (found[u]) m |= 1ull << who[u];
+                ans |= wave_or(m);
+                pdone += min(rem, max(0, 256 - pex));   // this step took pairs pex .. 255
+            }
+            ydone += min(yrem, max(0, 64 - yex));       // this chunk took y's yex .. 63
+        }
+        if (mine < total) ws.status[mat] = ((ans >> lane) & 1) ? ST_ANS : ST_NON;
+        flush_tally(tl, stats, uni(b), lane, 2);
+    }
+}
+
 __device__ __forceinline__ void ht_insert(int32_t* tv, int32_t* tj, uint32_t mask, int shift,
                                           int32_t c, int32_t j)
 {
@@ -1615,7 +1766,10 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         }
         if (!(parts & NEG_REST)) continue;
         prof_mark(1, r, false, st);
-        k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
+        if constexpr (QT == Q3P)
+            k_heavy3<T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
+        else
+            k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         if ((rc = check_launch(err))) return rc;
         prof_mark(1, r, true, st);
         if (j_end <= 64 * CK) {
@@ -1791,7 +1945,10 @@ int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out
     k_candidates<QT, NoTally, true><<<max(p.batch, 1), CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
                                                                      p.n_neg);
     if ((rc = check_launch(err))) return rc;
-    k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
+    if constexpr (QT == Q3P)
+        k_heavy3<NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
+    else
+        k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
     if ((rc = check_launch(err))) return rc;
     k_pack<<<(p.batch + 3) / 4 < PERSIST_BLOCKS ? (p.batch + 3) / 4 : PERSIST_BLOCKS, 256, 0, st>>>(
         p, ws, mask, q.n_valid);
