@@ -357,7 +357,18 @@ def profile_commands(config, steps):
         "python3 -u bench.py --copy-calibration 1024",
         f"rocprofv3 --pmc WRITE_SIZE -d {d}/copy_write -o copy --output-format csv -- "
         "python3 -u bench.py --copy-calibration 1024",
+        f"rocprofv3 --pmc {' '.join(L2_COUNTERS)} -d {d}/l2 -o bench --output-format csv -- {run} "
+        "--steps 3 --warmup 1",
+        f"rocprofv3 --pmc {' '.join(SQ_COUNTERS)} -d {d}/sq -o bench --output-format csv -- {run} "
+        "--steps 3 --warmup 1",
     ]
+
+
+# counter passes beside FETCH_SIZE / WRITE_SIZE (each within one pass's limits:
+# at most 4 TCC and 8 SQ counters)
+L2_COUNTERS = ("TCC_HIT_sum", "TCC_MISS_sum", "TCC_EA0_RDREQ_128B_sum", "TCC_EA0_RDREQ_DRAM_sum")
+SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_INST_ANY", "SQ_INSTS_VALU",
+               "SQ_INSTS_VMEM_RD", "SQ_INSTS_LDS")
 
 
 def summarize_profiles(config, folder, steps):
@@ -387,24 +398,29 @@ def summarize_profiles(config, folder, steps):
         parts = [x.strip() for x in targs.split(",")]
         if k in ("k_compact_reg", "k_positive"):   # templated on a count, not a shape
             return f"{k}<{parts[0]}>"
+        if k == "k_heavy3":                          # the 3p long-list kernel
+            return "k_heavy<3p" + (", accounting" if "NoTally" not in parts[0] else "") + ">"
         qt = SHAPES[int(parts[0])] if parts[0].isdigit() else parts[0]
         acct = any("Tally" in x and "NoTally" not in x for x in parts)
         shared = any(x == "true" for x in parts)
         return f"{k}<{qt}{', accounting' if acct else ''}{', given candidates' if shared else ''}>"
 
     def tagged(rows):
-        out, rnd = [], defaultdict(lambda: -1)
+        # one round per dispatch (a counter pass has a row per counter)
+        out, rnd, seen = [], defaultdict(lambda: -1), {}
         for r in sorted(rows, key=lambda r: int(r["Dispatch_Id"])):
             n = kname(r["Kernel_Name"])
             if n is None:
                 continue
-            shape = n[n.index("<") + 1:].split(",")[0].rstrip(">") if "<" in n else None
-            if n.startswith(("k_prepare", "k_no_draws")):
-                rnd[shape] = -1
-            if n.startswith("k_candidates"):
-                rnd[shape] += 1
-            rr = rnd[shape] if n.startswith(("k_candidates", "k_heavy")) else None
-            out.append((n, rr, r))
+            did = r["Dispatch_Id"]
+            if did not in seen:
+                shape = n[n.index("<") + 1:].split(",")[0].rstrip(">") if "<" in n else None
+                if n.startswith(("k_prepare", "k_no_draws")):
+                    rnd[shape] = -1
+                if n.startswith("k_candidates"):
+                    rnd[shape] += 1
+                seen[did] = rnd[shape] if n.startswith(("k_candidates", "k_heavy")) else None
+            out.append((n, seen[did], r))
         return out
 
     trace = list(csv.DictReader(open(one("**/*kernel_trace.csv"))))
@@ -480,6 +496,27 @@ def summarize_profiles(config, folder, steps):
         if k[1] in (0, None) and "accounting" not in k[0]:
             txt.append("kernel: %s | fetch_kib %.1f | write_kib %.1f | hbm_bytes_per_launch %d"
                        % (k[0] + ("" if k[1] is None else " r%d" % k[1]), f, w, hb))
+    # L2 and wavefront counters, when those passes were run: one row per kernel
+    # and round (first round only), a column per counter
+    for tag, names, title in (("l2", L2_COUNTERS, "L2 requests"),
+                              ("sq", SQ_COUNTERS, "Wavefront counters")):
+        got = sorted(glob.glob(os.path.join(folder, f"{tag}/**/*counter_collection.csv"), recursive=True))
+        if not got:
+            continue
+        a = defaultdict(list)
+        for n, rr, r in tagged(list(csv.DictReader(open(got[0])))):
+            a[(n, rr, r["Counter_Name"])].append(float(r["Counter_Value"]))
+        rowkeys = sorted({(n, rr) for n, rr, _ in a if rr in (0, None) and "accounting" not in n
+                          and not n.startswith(GRAPH_BUILD_KERNELS)},
+                         key=lambda k: -sum(dur.get(k, [0])))
+        L += [f"## {title} (per dispatch, averaged over the launches of each group)\n",
+              "| kernel | round | " + " | ".join(names) + " |",
+              "|---|---|" + "---|" * len(names)]
+        for n, rr in rowkeys:
+            vals = [a.get((n, rr, c)) for c in names]
+            L.append("| %s | %s | " % (n, "" if rr is None else rr) +
+                     " | ".join("%.4g" % (sum(v) / len(v)) if v else "-" for v in vals) + " |")
+        L.append("")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     md = os.path.join(ROOT, "profiles", f"negatives_{config}_trace_and_counters.md")
     with open(md, "w") as fh:
@@ -522,9 +559,13 @@ def main():
     ap.add_argument("--split", action="store_true",
                     help="candidate kernels of all shapes back to back on one stream "
                          "(smore_sample_negatives_part); the rest on each shape's stream")
-    ap.add_argument("--prepare-ahead", action="store_true",
-                    help="with one stream per shape, let a shape's preparation run before the "
-                         "wait for the previous candidate kernel (smore_wait_before_kernel)")
+    ap.add_argument("--wait-before-prepare", action="store_true",
+                    help="a shape's negatives wait for the previous candidate kernel of the chain "
+                         "before their preparation (default: only right before their candidate "
+                         "kernel, smore_wait_before_kernel, so the preparation runs ahead)")
+    ap.add_argument("--isolated-steps", type=int, default=6,
+                    help="after the timed steps, calls of each shape alone on one stream "
+                         "(per-shape rates; the first is a warm-up)")
     ap.add_argument("--pipeline", type=int, default=3,
                     help="sets of streams and outputs per shape that consecutive steps alternate "
                          "between (1: one stream per shape)")
@@ -538,6 +579,7 @@ def main():
     ap.add_argument("--print-profile-commands", action="store_true",
                     help="only print the rocprofv3 commands whose output --summarize reads")
     args = ap.parse_args()
+    args.prepare_ahead = not args.wait_before_prepare
 
     if args.print_profile_commands:
         print("\n".join(profile_commands(args.config, args.steps)))
@@ -765,6 +807,31 @@ def main():
         del ref
     log("schedule check: every shape's rows equal those of a plain call")
 
+    # each shape alone (one stream, nothing else running), on new query ids:
+    # per-shape rates and kernel durations without the other shapes' work
+    isolated = {}
+    for i, qt in enumerate(types):
+        rows = []
+        for k in range(args.isolated_steps):
+            off = (args.warmup + args.steps + i * args.isolated_steps + k) * B
+            a = sm.make_args(B, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries, query_offset=off)
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(8)]
+            e[0].record(stream)
+            sm.sample_positives(g, dags[qt], a, outs[qt], stream)
+            e[1].record(stream)
+            sm.profile_kernel(e[3], e[4], sm.KERNEL_CANDIDATES)
+            sm.profile_kernel(e[6], e[7], sm.KERNEL_HEAVY)
+            sm.sample_negatives(g, dags[qt], a, outs[qt], None, stream)
+            e[2].record(stream)
+            rows.append(e)
+        torch.cuda.synchronize()
+        rows = rows[1:] if len(rows) > 1 else rows      # the first call warms this shape up
+        ms = lambda x, y: float(np.mean([r[x].elapsed_time(r[y]) for r in rows]))
+        isolated[qt] = {"ms": ms(0, 2), "positive_ms": ms(0, 1), "candidate_kernel_ms": ms(3, 4),
+                        "long_list_kernel_ms": ms(6, 7)}
+        isolated[qt]["queries_per_s"] = B / (isolated[qt]["ms"] / 1e3)
+        log(f"{qt} alone: {isolated[qt]}")
+
     og = None
     if not (args.no_cpu_baseline and args.no_oracle_lines):
         import oracle
@@ -787,6 +854,10 @@ def main():
         per_type[qt] = {
             "queries_per_s": B / ((pos + neg) / 1e3) if rated else None,
             "complete_queries_per_s": a["complete"] / ((pos + neg) / 1e3) if rated else None,
+            "alone_queries_per_s": isolated[qt]["queries_per_s"],
+            "alone_ms": isolated[qt]["ms"],
+            "alone_candidate_kernel_ms": isolated[qt]["candidate_kernel_ms"],
+            "alone_long_list_kernel_ms": isolated[qt]["long_list_kernel_ms"],
             "positive_ms": pos, "negative_stage_ms": neg, "candidate_kernel_ms": cand,
             "long_list_kernel_ms": heavy,
             "draws_per_query": a["draws"] / max(a["valid"], 1),
