@@ -602,16 +602,27 @@ constexpr int CWG = 64;
 constexpr int HEAVY_WG = 256;    // threads of the heavy-queue workgroups
 constexpr int QF = 8;            // int32 per query in the per-query block
 constexpr int PERSIST_BLOCKS = 2048;
+// 3p long-list work in bounded units: the long-list kernel expands at most
+// UNIT_Y entities y of an item and searches at most UNIT_PAIRS pairs of one
+// y itself; the rest become units of the unit queue (UNITS_PER_QUERY slots
+// per query), which the unit kernel then takes, so one huge item is spread
+// over many wavefronts instead of setting the kernel's length alone.
+constexpr int UNIT_Y = 256;
+constexpr int UNIT_PAIRS = 1024;
+constexpr int UNITS_PER_QUERY = 64;
 
 // Workspace carved out of the caller's buffer.
 struct Ws {
     int32_t* ctrl;    // [0] queue pushes [1] queue pops [2 + k] size of active list k
+                      // [5] 3p units pushed
     int32_t* qf;      // [B][QF]: list k at [2k, 2k+1) edge range; [6] bit k: list k staged
     int32_t* cval;    // [B][neg_tries] candidate ids
     uint8_t* status;  // [B][neg_tries] ST_*
     int32_t* act[2];  // active query lists
     int2* queue;      // (query, draw) items
     int64_t qcap;
+    int4* units;      // 3p long-list units: (item, a, b, kind), counted by ctrl[5]
+    int64_t ucap;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -662,6 +673,8 @@ size_t ws_layout(const SampleParams& p, Ws* w, char* base)
     x.act[1] = (int32_t*)take((size_t)B * sizeof(int32_t));
     x.qcap = B * (int64_t)max_round_len(p);
     x.queue = (int2*)take((size_t)x.qcap * sizeof(int2));
+    x.ucap = B * (int64_t)UNITS_PER_QUERY;
+    x.units = (int4*)take((size_t)x.ucap * sizeof(int4));
     if (w) *w = x;
     return off;
 }
@@ -966,6 +979,7 @@ __global__ __launch_bounds__(256) void k_prepare(GraphView g, SampleParams p, sm
         ws.ctrl[1] = 0;
         ws.ctrl[2] = p.batch;
         ws.ctrl[3] = 0;
+        ws.ctrl[5] = 0;
     }
     int32_t anc[3], rel[3];
     int32_t* q = ws.qf + (int64_t)b * QF;
@@ -1365,17 +1379,180 @@ __device__ __forceinline__ uint64_t wave_or(uint64_t x)
     return x;
 }
 
+// A slice of one queued 3p item, held by one lane: the item's draw (its
+// query b and state index mat), relation r1, forward list F0 = A_r0(a0)
+// (edges [f0b, f0b + f0n)), the candidate's list S = R_r2(c) (edges from
+// sx), the range [y0, y1) of S's entities to expand and, for each of them,
+// the range [k0, k1) of its (y, key) pairs to search (keys from the shorter
+// of R_r1(y) and F0).
+struct Slice3 {
+    bool valid = false;
+    int32_t b = -1;
+    int64_t mat = 0;
+    int32_t r1 = 0, f0b = 0, f0n = 0, sx = 0, y0 = 0, y1 = 0, k0 = 0, k1 = 0;
+};
+
+// Reserve n unit slots for a wavefront (all lanes call it with the same n):
+// the first slot, or -1 when the queue is full, in which case the slots of
+// the failed reservation that lie inside the queue are marked unused.
+__device__ __forceinline__ int64_t reserve_units(Ws& ws, int32_t n, int lane)
+{
+    int32_t base = INT_MAX;
+    // once the queue is full the counter is left alone (it cannot grow without bound)
+    if (lane == 0 && ws.ctrl[5] < ws.ucap) base = atomicAdd(&ws.ctrl[5], n);
+    base = uni(__shfl(base, 0));
+    if ((int64_t)base + n <= ws.ucap) return base;
+    for (int64_t k = (int64_t)base + lane; k < ws.ucap; k += 64) ws.units[k] = make_int4(-1, 0, 0, 2);
+    return -1;
+}
+
+// Decide the slices of a wavefront, one per lane: the entities y of all of
+// them expanded 64 at a time (signature class, then the group under r1),
+// and the (y, key) pairs of all of them searched 256 at a time; a hit makes
+// its slice's item an answer, whose remaining y's and pairs are dropped,
+// the rest being laid out again after every step.  With PUSH (the
+// long-list kernel), y's beyond the first UNIT_Y of a slice and pairs
+// beyond the first UNIT_PAIRS of one y go to the unit queue (item index q)
+// when it has room, else they are decided here.  Returns the answer bits.
+template <bool PUSH, class T>
+__device__ uint64_t decide_slices3(const GraphView& g, Ws& ws, Slice3 w, int64_t q, int lane, T& tl)
+{
+    if constexpr (PUSH) {
+        const int32_t ny = w.valid ? w.y1 - w.y0 : 0;
+        const int32_t nu = ny > UNIT_Y ? (ny - UNIT_Y + UNIT_Y - 1) / UNIT_Y : 0;
+        int32_t tot;
+        const int32_t ex = excl_prefix(nu, lane, &tot);
+        if (tot > 0) {
+            const int64_t at = reserve_units(ws, tot, lane);
+            if (at >= 0) {
+                for (int32_t k = 0; k < nu; ++k) {
+                    const int32_t a = w.y0 + UNIT_Y * (k + 1);
+                    ws.units[at + ex + k] = make_int4((int32_t)q, a, min(a + UNIT_Y, w.y1), 0);
+                }
+                if (nu > 0) w.y1 = w.y0 + UNIT_Y;
+            }
+        }
+    }
+    uint64_t ans = 0;     // bit i: the item of lane i is an answer
+    int32_t ydone = 0;    // y's of this lane's slice expanded so far
+    for (;;) {
+        const int32_t yrem = (!w.valid || ((ans >> lane) & 1)) ? 0 : (w.y1 - w.y0) - ydone;
+        int32_t ytotal;
+        const int32_t yex = excl_prefix(yrem, lane, &ytotal);
+        if (ytotal == 0) break;
+        const int it = owner_lane(min(lane, ytotal - 1), yex);
+        const int32_t ypos = __shfl(w.y0, it) + __shfl(ydone, it) + lane - __shfl(yex, it);
+        const int32_t isx = __shfl(w.sx, it), ir1 = __shfl(w.r1, it);
+        const int32_t if0b = __shfl(w.f0b, it), if0n = __shfl(w.f0n, it);
+        int32_t k0 = __shfl(w.k0, it), k1 = __shfl(w.k1, it);
+        int2 s2 = make_int2(0, 0);
+        if (lane < ytotal) {
+            // y without an in-edge under r1's signature class has none under r1
+            const int32_t y = g.rev.nbr[isx + ypos];
+            tl.read(g.rev.nbr + isx + ypos, 4);
+            tl.read(g.sig + y, 1);
+            if (g.sig[y] & sig_bit(ir1)) s2 = group_range(g.rev, y, ir1, tl);
+        }
+        const int32_t len = s2.y - s2.x;
+        const bool kil = len <= if0n;            // search R_r1(y)'s entries in F0
+        const int32_t nall = len > 0 ? min(len, if0n) : 0;
+        if constexpr (PUSH) {
+            // pairs beyond the first UNIT_PAIRS of a y: units of UNIT_PAIRS keys
+            const int32_t nu = nall > UNIT_PAIRS ? (nall - 1) / UNIT_PAIRS : 0;
+            if (__ballot(nu > 0)) {
+                int32_t tot;
+                const int32_t ex = excl_prefix(nu, lane, &tot);
+                const int64_t at = reserve_units(ws, tot, lane);
+                if (at >= 0) {
+                    const int32_t iq = __shfl((int32_t)q, it);
+                    for (int32_t k = 0; k < nu; ++k)
+                        ws.units[at + ex + k] = make_int4(iq, ypos, UNIT_PAIRS * (k + 1), 1);
+                    if (nu > 0) k1 = UNIT_PAIRS;
+                }
+            }
+        }
+        const int32_t kb = min(k0, nall), ke = min(k1, nall);   // this y's keys [kb, ke)
+        int32_t pdone = 0;
+        for (;;) {
+            const int32_t rem = ((ans >> it) & 1) ? 0 : ke - kb - pdone;
+            int32_t ptotal;
+            const int32_t pex = excl_prefix(rem, lane, &ptotal);
+            if (ptotal == 0) break;
+            const int32_t* Bk[4];
+            int32_t nbk[4], x[4], who[4];
+            bool cnt[4], found[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t pi = 64 * u + lane;
+                const int32_t pq = pi < ptotal ? pi : ptotal - 1;
+                const int yl = owner_lane(pq, pex);
+                const int32_t off = __shfl(kb, yl) + __shfl(pdone, yl) + pq - __shfl(pex, yl);
+                const int32_t lx = __shfl(s2.x, yl), ln = __shfl(len, yl);
+                const int32_t k_in_l = __shfl((int32_t)kil, yl);
+                const int32_t fb = __shfl(if0b, yl), fn = __shfl(if0n, yl);
+                who[u] = __shfl(it, yl);
+                Bk[u] = g.fwd.nbr + fb;
+                nbk[u] = 0;
+                x[u] = -1;
+                cnt[u] = false;
+                if (pi < ptotal) {
+                    if (k_in_l) {
+                        x[u] = g.rev.nbr[lx + off];
+                        tl.read(g.rev.nbr + lx + off, 4);
+                        nbk[u] = fn;
+                    } else {
+                        x[u] = g.fwd.nbr[fb + off];
+                        Bk[u] = g.rev.nbr + lx;
+                        nbk[u] = ln;
+                        cnt[u] = true;
+                    }
+                }
+            }
+            search4v(Bk, nbk, x, cnt, found, tl);
+            uint64_t m = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (found[u]) m |= 1ull << who[u];
+            ans |= wave_or(m);
+            pdone += min(rem, max(0, 256 - pex));   // this step took pairs pex .. 255
+        }
+        ydone += min(yrem, max(0, 64 - yex));       // this chunk took y's yex .. 63
+    }
+    return ans;
+}
+
+// The slice of queued item qi: the whole list S, all keys.
+template <class T>
+__device__ __forceinline__ Slice3 item_slice3(const GraphView& g, const SampleParams& p,
+                                              const smore_sample_out& out, const Ws& ws, int64_t qi, T& tl)
+{
+    Slice3 w;
+    const int2 it = ws.queue[qi];
+    w.valid = true;
+    w.b = it.x;
+    w.mat = (int64_t)it.x * p.neg_tries + it.y;
+    const int32_t c = ws.cval[w.mat];
+    w.r1 = out.relations[3 * (int64_t)w.b + 1];
+    const int32_t r2 = out.relations[3 * (int64_t)w.b + 2];
+    const int32_t* qb = ws.qf + (int64_t)w.b * QF;
+    w.f0b = qb[0];
+    w.f0n = qb[1] - w.f0b;
+    const int2 S = group_range(g.rev, c, r2, tl);
+    w.sx = S.x;
+    w.y0 = 0;
+    w.y1 = S.y - S.x;
+    w.k0 = 0;
+    w.k1 = INT_MAX;
+    return w;
+}
+
 // The long-list kernel of 3p, batched: wavefront w takes items w,
 // w + nwaves, ... like k_heavy, but decides up to 64 of them together, one
-// per lane.  The entities y of all their candidates' lists R_r2(c) are
-// expanded 64 at a time (signature class, then the group under r1), and
-// the (y, key) pairs of all of them, keys from the shorter of R_r1(y) and
-// the item's F0 = A_r0(a0), are searched 256 at a time; a hit makes its
-// item an answer, and an item's remaining y's are skipped once it is one.
-// A wavefront holds a few items (the queue over the persistent grid), so
-// their dependent chains overlap instead of running one item after the
-// other.  With the read tally, a batch's reads are charged to the query of
-// its first item (the sums over all queries are exact).
+// per lane (decide_slices3), so their dependent chains overlap instead of
+// running one item after the other; the parts of huge items go to the unit
+// queue.  It writes every item's state.  With the read tally, a batch's
+// reads are charged to the query of its first item (the sums over all
+// queries are exact).
 template <class T>
 __global__ __launch_bounds__(HEAVY_WG) void k_heavy3(GraphView g, SampleParams p, smore_sample_out out,
                                                      Ws ws, int64_t* stats, int nxt)
@@ -1387,97 +1564,51 @@ __global__ __launch_bounds__(HEAVY_WG) void k_heavy3(GraphView g, SampleParams p
     const int32_t w0 = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6));
     T tl;
     for (int64_t base = w0; base < total; base += 64 * (int64_t)nwaves) {
-        // this lane's item: candidate list S = R_r2(c), relation r1, F0
         const int64_t mine = base + (int64_t)lane * nwaves;
-        int32_t b = -1, r1 = 0, f0b = 0, f0n = 0;
-        int64_t mat = 0;
-        int2 S = make_int2(0, 0);
+        Slice3 w;
+        if (mine < total) w = item_slice3(g, p, out, ws, mine, tl);
+        const uint64_t ans = decide_slices3<true>(g, ws, w, mine, lane, tl);
+        if (mine < total) ws.status[w.mat] = ((ans >> lane) & 1) ? ST_ANS : ST_NON;
+        flush_tally(tl, stats, uni(__shfl(w.b, 0)), lane, 2);
+    }
+}
+
+// The units the long-list kernel left: wavefront w takes units w,
+// w + nwaves, ..., up to 64 at a time, one per lane; a unit of an item
+// already decided an answer is skipped, and a hit makes its item an answer
+// (units never clear a state, so their order does not matter).
+template <class T>
+__global__ __launch_bounds__(HEAVY_WG) void k_units3(GraphView g, SampleParams p, smore_sample_out out,
+                                                     Ws ws, int64_t* stats)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t total = uni((int32_t)min((int64_t)ws.ctrl[5], ws.ucap));
+    const int32_t nwaves = gridDim.x * (HEAVY_WG / 64);
+    const int32_t w0 = uni(blockIdx.x * (HEAVY_WG / 64) + (threadIdx.x >> 6));
+    T tl;
+    for (int64_t base = w0; base < total; base += 64 * (int64_t)nwaves) {
+        const int64_t mine = base + (int64_t)lane * nwaves;
+        Slice3 w;
         if (mine < total) {
-            const int2 it = ws.queue[mine];
-            b = it.x;
-            mat = (int64_t)it.x * p.neg_tries + it.y;
-            const int32_t c = ws.cval[mat];
-            r1 = out.relations[3 * (int64_t)b + 1];
-            const int32_t r2 = out.relations[3 * (int64_t)b + 2];
-            const int32_t* qb = ws.qf + (int64_t)b * QF;
-            f0b = qb[0];
-            f0n = qb[1] - f0b;
-            S = group_range(g.rev, c, r2, tl);
-        }
-        uint64_t ans = 0;     // bit i: the item of lane i is an answer
-        int32_t ydone = 0;    // y's of this lane's item expanded so far
-        // the y's of the items not yet answers, 64 at a time, laid out again
-        // after every chunk
-        for (;;) {
-            const int32_t yrem = ((ans >> lane) & 1) ? 0 : (S.y - S.x) - ydone;
-            int32_t ytotal;
-            const int32_t yex = excl_prefix(yrem, lane, &ytotal);
-            if (ytotal == 0) break;
-            const int it = owner_lane(min(lane, ytotal - 1), yex);
-            const int32_t ipos = __shfl(ydone, it) + lane - __shfl(yex, it);   // y index in its item
-            const int32_t iSx = __shfl(S.x, it), ir1 = __shfl(r1, it);
-            const int32_t if0b = __shfl(f0b, it), if0n = __shfl(f0n, it);
-            int2 s2 = make_int2(0, 0);
-            if (lane < ytotal) {
-                // y without an in-edge under r1's signature class has none under r1
-                const int32_t y = g.rev.nbr[iSx + ipos];
-                tl.read(g.rev.nbr + iSx + ipos, 4);
-                tl.read(g.sig + y, 1);
-                if (g.sig[y] & sig_bit(ir1)) s2 = group_range(g.rev, y, ir1, tl);
-            }
-            const int32_t len = s2.y - s2.x;
-            const bool kil = len <= if0n;            // search R_r1(y)'s entries in F0
-            const int32_t npair = len > 0 ? min(len, if0n) : 0;
-            // pairs 256 at a time over the y's whose item is not yet an
-            // answer: after each step the remaining pairs are laid out again
-            int32_t pdone = 0;                        // this y's pairs searched so far
-            for (;;) {
-                const int32_t rem = ((ans >> it) & 1) ? 0 : npair - pdone;
-                int32_t ptotal;
-                const int32_t pex = excl_prefix(rem, lane, &ptotal);
-                if (ptotal == 0) break;
-                const int32_t* Bk[4];
-                int32_t nbk[4], x[4], who[4];
-                bool cnt[4], found[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int32_t pi = 64 * u + lane;
-                    const int32_t pq = pi < ptotal ? pi : ptotal - 1;
-                    const int yl = owner_lane(pq, pex);
-                    const int32_t off = __shfl(pdone, yl) + pq - __shfl(pex, yl);
-                    const int32_t lx = __shfl(s2.x, yl), ln = __shfl(len, yl);
-                    const int32_t k_in_l = __shfl((int32_t)kil, yl);
-                    const int32_t fb = __shfl(if0b, yl), fn = __shfl(if0n, yl);
-                    who[u] = __shfl(it, yl);
-                    Bk[u] = g.fwd.nbr + fb;
-                    nbk[u] = 0;
-                    x[u] = -1;
-                    cnt[u] = false;
-                    if (pi < ptotal) {
-                        if (k_in_l) {
-                            x[u] = g.rev.nbr[lx + off];
-                            tl.read(g.rev.nbr + lx + off, 4);
-                            nbk[u] = fn;
-                        } else {
-                            x[u] = g.fwd.nbr[fb + off];
-                            Bk[u] = g.rev.nbr + lx;
-                            nbk[u] = ln;
-                            cnt[u] = true;
-                        }
-                    }
+            const int4 u = ws.units[mine];
+            if (u.w != 2) {
+                w = item_slice3(g, p, out, ws, u.x, tl);
+                if (ws.status[w.mat] == ST_ANS) {
+                    w.valid = false;
+                } else if (u.w == 0) {           // entities [a, b) of S, all keys
+                    w.y0 = u.y;
+                    w.y1 = u.z;
+                } else {                         // entity a of S, keys [b, b + UNIT_PAIRS)
+                    w.y0 = u.y;
+                    w.y1 = u.y + 1;
+                    w.k0 = u.z;
+                    w.k1 = u.z + UNIT_PAIRS;
                 }
-                search4v(Bk, nbk, x, cnt, found, tl);
-                uint64_t m = 0;
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (found[u]) m |= 1ull << who[u];
-                ans |= wave_or(m);
-                pdone += min(rem, max(0, 256 - pex));   // this step took pairs pex .. 255
             }
-            ydone += min(yrem, max(0, 64 - yex));       // this chunk took y's yex .. 63
         }
-        if (mine < total) ws.status[mat] = ((ans >> lane) & 1) ? ST_ANS : ST_NON;
-        flush_tally(tl, stats, uni(b), lane, 2);
+        const uint64_t ans = decide_slices3<false>(g, ws, w, -1, lane, tl);
+        if (w.valid && ((ans >> lane) & 1)) ws.status[w.mat] = ST_ANS;
+        flush_tally(tl, stats, uni(__shfl(max(w.b, 0), 0)), lane, 2);
     }
 }
 
@@ -1521,7 +1652,7 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out
     const uint32_t tmask = (uint32_t)tcap - 1;
     const int32_t nact = uni(ws.ctrl[2 + cur]);
     // the heavy queue of this round is drained: ready it for the next round
-    if (blockIdx.x == 0 && lane == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
+    if (blockIdx.x == 0 && lane == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; ws.ctrl[5] = 0; }
     for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
         const int32_t b = uni(ws.act[cur][qi]);
         if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
@@ -1590,7 +1721,7 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
     const uint64_t below = lanes_below(lane);
     const uint32_t tmask = (uint32_t)tcap - 1;
     const int32_t nact = uni(ws.ctrl[2 + cur]);
-    if (blockIdx.x == 0 && threadIdx.x == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; }
+    if (blockIdx.x == 0 && threadIdx.x == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; ws.ctrl[5] = 0; }
     const int32_t nk = uni((j_end + 63) >> 6);
     for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
         const int32_t b = ident ? qi : uni(ws.act[cur][qi]);
@@ -1766,10 +1897,13 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         }
         if (!(parts & NEG_REST)) continue;
         prof_mark(1, r, false, st);
-        if constexpr (QT == Q3P)
+        if constexpr (QT == Q3P) {
             k_heavy3<T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
-        else
+            if ((rc = check_launch(err))) return rc;
+            k_units3<T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats);
+        } else {
             k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
+        }
         if ((rc = check_launch(err))) return rc;
         prof_mark(1, r, true, st);
         if (j_end <= 64 * CK) {
@@ -1945,10 +2079,13 @@ int run_pairs(const GraphView& gv, const SampleParams& p, const smore_sample_out
     k_candidates<QT, NoTally, true><<<max(p.batch, 1), CWG, 0, st>>>(gv, p, q, ws, nullptr, 0, 0,
                                                                      p.n_neg);
     if ((rc = check_launch(err))) return rc;
-    if constexpr (QT == Q3P)
+    if constexpr (QT == Q3P) {
         k_heavy3<NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
-    else
+        if ((rc = check_launch(err))) return rc;
+        k_units3<NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr);
+    } else {
         k_heavy<QT, NoTally><<<PERSIST_BLOCKS, HEAVY_WG, 0, st>>>(gv, p, q, ws, nullptr, 1);
+    }
     if ((rc = check_launch(err))) return rc;
     k_pack<<<(p.batch + 3) / 4 < PERSIST_BLOCKS ? (p.batch + 3) / 4 : PERSIST_BLOCKS, 256, 0, st>>>(
         p, ws, mask, q.n_valid);

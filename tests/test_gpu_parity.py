@@ -427,3 +427,36 @@ def test_gather_probe_reads_the_table():
     s = sm.gather_probe(t, 1 << 16)
     torch.cuda.synchronize()
     assert (s != 0).any()
+
+
+def hub_graph_3p():
+    """Two mirrored components for 3p: anchor 0 -(r0)-> x (1,200 entities)
+    -(r1, complete)-> y (400) -(r2, complete)-> c (100), and anchor 1 with
+    x', y', c' alike.  A candidate c or c' has 400 in-neighbours under r2
+    and each of them 1,200 under r1, against a forward list of 1,200 (too
+    long to stage): its long-list work is split into units of entities and
+    of keys, which are answers in one component and non-answers in the
+    other."""
+    x, xp = np.arange(10, 1210), np.arange(1210, 2410)
+    y, yp = np.arange(2500, 2900), np.arange(2900, 3300)
+    c, cp = np.arange(3500, 3600), np.arange(3600, 3700)
+    parts = [np.stack([np.zeros_like(x), np.zeros_like(x), x], 1),
+             np.stack([np.ones_like(xp), np.zeros_like(xp), xp], 1)]
+    for a, b, r in ((x, y, 1), (xp, yp, 1), (y, c, 2), (yp, cp, 2)):
+        aa, bb = np.meshgrid(a, b, indexing="ij")
+        parts.append(np.stack([aa.ravel(), np.full(aa.size, r), bb.ravel()], 1))
+    return np.concatenate(parts).astype(np.int32), 4000, 3
+
+
+def test_3p_long_list_units_on_hub_graph():
+    tr, V, R = hub_graph_3p()
+    g, og = graph_pair(tr, V, R)
+    for seed in (1, 2):
+        progress(f"3p hub units seed {seed}")
+        got = gpu_sample(g, "3p", 300, 128, seed=seed, neg_tries=512)
+        ref = og.sample("3p", 300, 128, seed=seed, neg_tries=512)
+        assert_same(got, ref, what=f"3p hub seed {seed}")
+        assert (got["n_valid"] >= 0).sum() > 100
+        # candidates of the other component were drawn and verified
+        c_other = np.isin(got["negatives"], np.arange(3500, 3700)).sum()
+        assert c_other > 0
