@@ -945,19 +945,23 @@ int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const in
    - a neighbour list that is expanded: its entries in ascending order, up
      to the first one that decides the check;
    - a list met with a forward-cached set: the shorter side gives the keys
-     in ascending order (list keys are read, cached keys are free), each
-     key is looked up in the other side by the same lower-bound search
-     (probes of a list are read, of a cached set free), up to the first
-     common entity;
+     in ascending order, each key is looked up in the other side by the
+     same lower-bound search, up to the first common entity; list keys and
+     list probes are read; a cached set that fits the STAGE_BUDGET entries
+     staged per query (each cut set in node order is staged when it fits in
+     what the sets staged before it left of the budget) is held on chip, so its keys and probes are free,
+     while a larger one is searched where it is stored: the forward group
+     A_r(a) when the set is one projection of an anchor (the only kind the
+     strict cut caches), else a sorted array of its own;
    - forward caching: every cut set once, from the anchors, with the same
      reads (node entries, group search, the whole list).
    The candidates of query qid are draws j < n_draws, c_j =
    pick(U(NEG, qid, 0, j), V).  Lines fall in two parts: part 0 holds the
    forward caching, each candidate's own node entries and group search,
    edge tests against an anchor, and the expansion of backward lists of at
-   most LONG_LIST entries when every forward-cached set of the query fits
-   the STAGE_BUDGET entries staged per query; part 1 holds everything read
-   below a longer list or with a set that does not fit.  Each part counts
+   most LONG_LIST entries when every forward-cached set of the query is
+   staged; part 1 holds everything read below a longer list, and every
+   backward read of a query with a set that is not staged.  Each part counts
    its distinct lines; the total counts distinct lines over both. */
 #define LONG_LIST 8
 #define STAGE_BUDGET 1024
@@ -996,10 +1000,21 @@ typedef struct {
     const otype *T;
     uint32_t cut;
     iset F[8];
+    int staged[8];          /* cut set k fits the staging budget */
+    int64_t fbase[8];       /* first forward edge of an unstaged cut set that is
+                               one forward group, else -1 (an array of its own) */
     int all_staged;
     const int32_t *anchors, *relations;
     lineset part[2];
 } vlines;
+
+/* a read of entry i of cut set k where it is stored (unstaged sets only) */
+static void vset_read(vlines *L, int part, int k, int64_t i)
+{
+    if (L->staged[k]) return;
+    if (L->fbase[k] >= 0) ls_add(&L->part[part], L_FNBR, (L->fbase[k] + i) * 4, 4);
+    else ls_add(&L->part[part], 6 + k, i * 4, 4);
+}
 
 /* the group of relation r of entity v in one direction: [*b, *e), or 0 */
 static int vgroup(vlines *L, int part, int dir, int32_t v, int32_t r, int64_t *b, int64_t *e)
@@ -1023,18 +1038,30 @@ static int vgroup(vlines *L, int part, int dir, int32_t v, int32_t r, int64_t *b
     return 1;
 }
 
-/* does the reverse list [b, e) share an entity with the cached set F? */
-static int vmeet(vlines *L, int part, int64_t b, int64_t e, iset F)
+/* does the reverse list [b, e) share an entity with cut set k? */
+static int vmeet(vlines *L, int part, int64_t b, int64_t e, int k_set)
 {
     const int32_t *nbr = L->g->r_nbr;
+    const iset F = L->F[k_set];
     if (e - b <= F.n) {
         for (int64_t i = b; i < e; i++) {
             ls_add(&L->part[part], L_RNBR, i * 4, 4);
-            if (set_has(F, nbr[i])) return 1;
+            /* lower-bound search of the list's entry in the cached set */
+            int64_t lo = 0, hi = F.n;
+            while (lo < hi) {
+                const int64_t mid = lo + (hi - lo) / 2;
+                vset_read(L, part, k_set, mid);
+                if (F.v[mid] < nbr[i]) lo = mid + 1; else hi = mid;
+            }
+            if (lo < F.n) {
+                vset_read(L, part, k_set, lo);
+                if (F.v[lo] == nbr[i]) return 1;
+            }
         }
         return 0;
     }
     for (int64_t k = 0; k < F.n; k++) {
+        vset_read(L, part, k_set, k);
         int64_t lo = b, hi = e;
         while (lo < hi) {
             const int64_t mid = lo + (hi - lo) / 2;
@@ -1069,7 +1096,7 @@ static int vmember(vlines *L, int k, int32_t x, int part)
     const int ch = nd->ch[0];
     const int edge_test = (L->cut & (1u << ch)) && L->T->nd[ch].op == N_ANCHOR;
     const int p = edge_test ? part : (e - b > LONG_LIST || !L->all_staged) ? 1 : part;
-    if (L->cut & (1u << ch)) return vmeet(L, p, b, e, L->F[ch]);
+    if (L->cut & (1u << ch)) return vmeet(L, p, b, e, ch);
     for (int64_t i = b; i < e; i++) {
         ls_add(&L->part[p], L_RNBR, i * 4, 4);
         if (vmember(L, ch, L->g->r_nbr[i], p)) return 1;
@@ -1110,15 +1137,25 @@ int oracle_verify_lines(const okg *g, int qtype, const int32_t *anchors, const i
     L.g = g; L.T = T; L.cut = cut_mask; L.anchors = anchors; L.relations = relations;
     int64_t staged = 0;
     L.all_staged = 1;
-    for (int k = 0; k < T->n; k++)
-        if (cut_mask & (1u << k)) {
-            L.F[k] = eval_node(g, T, k, anchors, relations);
-            vforward(&L, k);
-            if (T->nd[k].op != N_ANCHOR) {
-                staged += L.F[k].n;
-                if (staged > STAGE_BUDGET) L.all_staged = 0;
+    for (int k = 0; k < T->n; k++) {
+        L.staged[k] = 1;
+        L.fbase[k] = -1;
+        if (!(cut_mask & (1u << k))) continue;
+        L.F[k] = eval_node(g, T, k, anchors, relations);
+        vforward(&L, k);
+        const onode *nd = &T->nd[k];
+        if (nd->op == N_ANCHOR) continue;
+        if (L.F[k].n <= STAGE_BUDGET - staged) staged += L.F[k].n;
+        else {
+            L.all_staged = 0;
+            L.staged[k] = 0;
+            if (nd->op == N_PROJ && T->nd[nd->ch[0]].op == N_ANCHOR) {
+                int64_t fb, fe;
+                rel_range(g->f_off, g->f_rel, anchors[T->nd[nd->ch[0]].slot], relations[nd->slot], &fb, &fe);
+                L.fbase[k] = fb;
             }
         }
+    }
     for (int32_t j = 0; j < n_draws; j++) {
         const int32_t c = (int32_t)oracle_pick(oracle_draw(seed, TAG_NEG, qid, 0, (uint32_t)j),
                                                (uint64_t)g->V);

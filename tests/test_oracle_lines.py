@@ -6,6 +6,8 @@ grp[S+1] int32 pairs, nbr[E] int32 per direction).
 * Hand graphs whose group and edge indices are written out here: the lines
   of every read follow from those indices and the byte offsets 4v, 8s and
   4e, so each expected line set is derived without the oracle's code.
+* A cached set one entry over the per-query staging budget is searched
+  where it is stored (its forward group), one entry under it is free.
 * Invariants on random graphs for all fourteen shapes: every draw reads its
   own node entries (a lower bound from the draws alone), the parts bound
   the total, a graph whose lists never exceed eight entries puts nothing in
@@ -95,6 +97,64 @@ def test_two_hop_long_list_goes_to_the_long_part(oracle_lib):
         part0 = len(fwd) + len(fgrp) + len(fnbr) + len(node) + len(grp)
         assert got[0].tolist() == [part0, len(nbr_long), part0 + len(nbr_long)], qid
         assert (100 in cs) == (len(nbr_long) == 1)
+
+
+# Probes of the lower-bound search of a key in F0 = {1..n_f} (entry i holds
+# i + 1), worked out by hand: key 3 ends at entry 2 and reads it once more;
+# keys 1105 and 1110 exceed every entry and end past the last one.
+PROBES = {
+    1025: {3: [512, 256, 128, 64, 32, 16, 8, 4, 2, 1, 2],
+           1105: [512, 769, 897, 961, 993, 1009, 1017, 1021, 1023, 1024]},
+}
+
+
+@pytest.mark.parametrize("n_f", [1024, 1025])
+def test_cached_set_over_the_staging_budget_is_searched_in_place(oracle_lib, n_f):
+    # 2p: anchor 0 -(r0)-> 1..n_f, 3 -(r1)-> 1150, 1105 and 1110 -(r1)-> 1151.
+    # The strict cut caches F0 = {1..n_f}: forward group 0 of entity 0,
+    # forward edges 0..n_f-1.  Reverse groups: entities 1..n_f -> groups
+    # 0..n_f-1 (relation 0), 1150 -> group n_f, 1151 -> group n_f+1 (both
+    # relation 1); reverse edges: tails 1..n_f -> edges 0..n_f-1, 1150 -> edge
+    # n_f (head 3), 1151 -> edges n_f+1, n_f+2 (heads 1105, 1110).  Both lists
+    # are shorter than F0, so their entries are the keys searched in F0.
+    # With 1,024 entries F0 is staged: the searches are free and the short
+    # lists are part 0.  With 1,025 it is not: every backward read is part 1
+    # and each probe of F0 reads its forward edge.
+    V = 1200
+    tr = [[0, 0, y] for y in range(1, n_f + 1)] + [[3, 1, 1150], [1105, 1, 1151], [1110, 1, 1151]]
+    g = oracle_lib.Graph(np.array(tr, np.int32), V, 2)
+    anchors, rels = np.array([[0, -1, -1]], np.int32), np.array([[0, 1, -1]], np.int32)
+    pos = np.array([1150], np.int32)
+    fnode = lines_of(0, 8)                          # forward node entries of 0
+    fgrp = lines_of(0, 4) | lines_of(4, 4) | lines_of(12, 4)
+    fnbr = lines_of(0, 4 * n_f)
+    n, seed = 4000, 3
+    seen = set()
+    for qid in range(4):
+        cs = draws(oracle_lib, seed, qid, n, V)
+        node, grp, rnbr, fprobe = set(), set(), set(), set()
+        for c in cs:
+            node |= lines_of(4 * c, 8)
+            if 1 <= c <= n_f:
+                grp |= lines_of(8 * (c - 1), 4)
+            elif c in (1150, 1151):
+                s_ = n_f + (c - 1150)
+                grp |= lines_of(8 * s_, 4) | lines_of(8 * s_ + 4, 4) | lines_of(8 * (s_ + 1) + 4, 4)
+                edges = [n_f] if c == 1150 else [n_f + 1, n_f + 2]
+                for e_ in edges:
+                    rnbr |= lines_of(4 * e_, 4)
+                if n_f in PROBES:
+                    for i in PROBES[n_f][3 if c == 1150 else 1105]:
+                        fprobe |= lines_of(4 * i, 4)
+                seen.add(c)
+        got = g.verify_lines("2p", anchors, rels, pos, strict_mask(oracle_lib, "2p"), seed, qid, n)
+        base = len(fnode) + len(fgrp) + len(fnbr) + len(node) + len(grp)
+        if n_f in PROBES:
+            assert fprobe <= fnbr
+            assert got[0].tolist() == [base, len(rnbr) + len(fprobe), base + len(rnbr)], qid
+        else:
+            assert got[0].tolist() == [base + len(rnbr), 0, base + len(rnbr)], qid
+    assert seen == {1150, 1151}
 
 
 @pytest.mark.parametrize("qt", ["1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up",
