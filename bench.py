@@ -398,8 +398,9 @@ def summarize_profiles(config, folder, steps):
         parts = [x.strip() for x in targs.split(",")]
         if k in ("k_compact_reg", "k_positive"):   # templated on a count, not a shape
             return f"{k}<{parts[0]}>"
-        if k == "k_heavy3":                          # the 3p long-list kernel
-            return "k_heavy<3p" + (", accounting" if "NoTally" not in parts[0] else "") + ">"
+        if k in ("k_heavy3", "k_units3"):            # the 3p long-list kernel and its units
+            return (("k_heavy<3p" if k == "k_heavy3" else "k_units<3p") +
+                    (", accounting" if "NoTally" not in parts[0] else "") + ">")
         qt = SHAPES[int(parts[0])] if parts[0].isdigit() else parts[0]
         acct = any("Tally" in x and "NoTally" not in x for x in parts)
         shared = any(x == "true" for x in parts)
@@ -419,7 +420,7 @@ def summarize_profiles(config, folder, steps):
                     rnd[shape] = -1
                 if n.startswith("k_candidates"):
                     rnd[shape] += 1
-                seen[did] = rnd[shape] if n.startswith(("k_candidates", "k_heavy")) else None
+                seen[did] = rnd[shape] if n.startswith(("k_candidates", "k_heavy", "k_units")) else None
             out.append((n, seen[did], r))
         return out
 
