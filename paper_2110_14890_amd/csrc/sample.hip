@@ -267,6 +267,46 @@ __device__ __forceinline__ void search4v(const int32_t* const* B, const int32_t*
     }
 }
 
+// search4v with three probes per step where four or more entries remain
+// (a quaternary search: fewer dependent reads, more reads in all).
+template <class T>
+__device__ __forceinline__ void search4q(const int32_t* const* B, const int32_t* nb, const int32_t* x,
+                                         const bool* count, bool* found, T& tl)
+{
+    int32_t base[4] = {0, 0, 0, 0}, n[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) n[k] = nb[k];
+    for (;;) {
+        bool more = false;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (n[k] >= 4) {
+                const int32_t q = n[k] >> 2;
+                const int32_t* b = B[k] + base[k];
+                if (count[k]) { tl.read(b + q, 4); tl.read(b + 2 * q, 4); tl.read(b + 3 * q, 4); }
+                const int32_t v1 = b[q], v2 = b[2 * q], v3 = b[3 * q];
+                base[k] += q * ((v1 <= x[k]) + (v2 <= x[k]) + (v3 <= x[k]));
+                n[k] -= 3 * q;
+            } else if (n[k] > 1) {
+                const int32_t half = n[k] >> 1;
+                if (count[k]) tl.read(B[k] + base[k] + half, 4);
+                base[k] = B[k][base[k] + half] <= x[k] ? base[k] + half : base[k];
+                n[k] -= half;
+            }
+            more |= n[k] > 1;
+        }
+        if (!more) break;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        found[k] = false;
+        if (nb[k] > 0) {
+            if (count[k]) tl.read(B[k] + base[k], 4);
+            found[k] = B[k][base[k]] == x[k];
+        }
+    }
+}
+
 // Does some element of K[0..nk) occur in L[0..nl)?  Whole wavefront, 256
 // keys per step (four per lane).  k_glob / l_glob: whether reads of the
 // list count as graph traffic.
@@ -1508,7 +1548,7 @@ __device__ uint64_t decide_slices3(const GraphView& g, Ws& ws, Slice3 w, int64_t
                     }
                 }
             }
-            search4v(Bk, nbk, x, cnt, found, tl);
+            search4q(Bk, nbk, x, cnt, found, tl);
             uint64_t m = 0;
 #pragma unroll
             for (int u = 0; u < 4; ++u)
