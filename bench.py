@@ -556,17 +556,19 @@ def main():
                          "GPU vs the exhaustive CPU oracle (2p, ip, pni)")
     ap.add_argument("--serial", action="store_true",
                     help="run the shapes of a step one after another on one stream "
-                         "(default: one stream per shape; a shape's negatives start when the "
-                         "previous shape's candidate kernel ends)")
-    ap.add_argument("--concurrent", action="store_true",
-                    help="no chain: the shapes' streams run each step without waiting for each other")
+                         "(default: one stream per shape, the shapes' streams running side by "
+                         "side without waiting for each other)")
+    ap.add_argument("--chained", action="store_true",
+                    help="chain the candidate kernels of all shapes and steps: a shape's "
+                         "candidate kernel starts when the previous one in the chain has ended")
     ap.add_argument("--split", action="store_true",
                     help="candidate kernels of all shapes back to back on one stream "
                          "(smore_sample_negatives_part); the rest on each shape's stream")
     ap.add_argument("--wait-before-prepare", action="store_true",
-                    help="a shape's negatives wait for the previous candidate kernel of the chain "
-                         "before their preparation (default: only right before their candidate "
-                         "kernel, smore_wait_before_kernel, so the preparation runs ahead)")
+                    help="with --chained: a shape's negatives wait for the previous candidate "
+                         "kernel of the chain before their preparation (else only right before "
+                         "their candidate kernel, smore_wait_before_kernel, so the preparation "
+                         "runs ahead)")
     ap.add_argument("--isolated-steps", type=int, default=6,
                     help="after the timed steps, calls of each shape alone on one stream "
                          "(per-shape rates; the first is a warm-up)")
@@ -583,7 +585,8 @@ def main():
     ap.add_argument("--print-profile-commands", action="store_true",
                     help="only print the rocprofv3 commands whose output --summarize reads")
     args = ap.parse_args()
-    args.prepare_ahead = not args.wait_before_prepare
+    args.concurrent = not (args.chained or args.serial or args.split)
+    args.prepare_ahead = args.chained and not args.wait_before_prepare
 
     if args.print_profile_commands:
         print("\n".join(profile_commands(args.config, args.steps)))
@@ -677,14 +680,15 @@ def main():
         log(f"{qt}: {acct[qt]}")
 
     # One stream per shape (default priority, a workspace each); each stream
-    # runs its shape's steps in order.  The candidate kernels of all shapes
-    # and steps form one chain (3p, ip, pi, the next step's 3p, ...): a
-    # shape's negatives start when the candidate kernel before it in the
-    # chain has ended (the event the library records after that kernel; with
-    # --prepare-ahead the library waits for it only after the shape's
-    # preparation), so each candidate kernel has the GPU mostly to itself
-    # while positives and the long-list and selection kernels of other
-    # shapes run beside it.
+    # runs its shape's steps in order, and by default the shapes' streams run
+    # side by side without waiting for each other.  With --chained the
+    # candidate kernels of all shapes and steps form one chain (3p, ip, pi,
+    # the next step's 3p, ...): a shape's negatives start when the candidate
+    # kernel before it in the chain has ended (the event the library records
+    # after that kernel; with prepare-ahead the library waits for it only
+    # after the shape's preparation), so each candidate kernel has the GPU
+    # mostly to itself while positives and the long-list and selection
+    # kernels of other shapes run beside it.
     # The streams join the timing stream only at the ends of the timed region.
     # With --split the chain needs no cross-stream waits: every shape's
     # first-round candidate kernel runs on one candidate stream, in chain
