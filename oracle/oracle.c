@@ -1162,8 +1162,8 @@ int oracle_verify_lines(const okg *g, int qtype, const int32_t *anchors, const i
         (void)vmember(&L, T->root, c, 0);
     }
     int64_t *all = (int64_t *)malloc((size_t)(L.part[0].n + L.part[1].n + 1) * 8);
-    memcpy(all, L.part[0].v, (size_t)L.part[0].n * 8);
-    memcpy(all + L.part[0].n, L.part[1].v, (size_t)L.part[1].n * 8);
+    if (L.part[0].n) memcpy(all, L.part[0].v, (size_t)L.part[0].n * 8);
+    if (L.part[1].n) memcpy(all + L.part[0].n, L.part[1].v, (size_t)L.part[1].n * 8);
     lines[0] = ls_distinct(L.part[0].v, L.part[0].n);
     lines[1] = ls_distinct(L.part[1].v, L.part[1].n);
     lines[2] = ls_distinct(all, L.part[0].n + L.part[1].n);

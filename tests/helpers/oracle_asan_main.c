@@ -6,10 +6,12 @@
  * query shape it runs sampling (with and without negatives, a draw budget
  * equal to n_neg, max_fanout), shared-candidate minibatches (empty and
  * non-empty sets), verification of given candidates (none, and candidates
- * out of range), the exhaustive answer set and the bidirectional check on
- * every node cut.  Every output array is printed as one line
- * "<case> <values...>" so that the test can compare it with the ordinary
- * build of the oracle called through its Python wrapper.
+ * out of range), the exhaustive answer set, the bidirectional check and the
+ * count of the lines it reads on every node cut, and the line count of a
+ * query whose cached set is just under and just over the staging budget.
+ * Every output array is printed as one line "<case> <values...>" so that
+ * the test can compare it with the ordinary build of the oracle called
+ * through its Python wrapper.
  */
 #include <stdio.h>
 #include <stdlib.h>
@@ -99,7 +101,15 @@ int main(void)
                     if (r < 0) { is_cut = 0; break; }
                     in[c] = r;
                 }
-                if (is_cut) put("bidir", name, (int)cut, in, V);
+                if (is_cut) {
+                    put("bidir", name, (int)cut, in, V);
+                    /* lines read by the check of 40 draws of this query */
+                    int64_t l64[3];
+                    if (oracle_verify_lines(g, ty, anc + 3 * b, rel + 3 * b, cut, 5, (uint32_t)b, 40, l64))
+                        return 7;
+                    const int32_t l32[4] = {b, (int32_t)l64[0], (int32_t)l64[1], (int32_t)l64[2]};
+                    put("lines", name, (int)cut, l32, 4);
+                }
             }
             free(in);
             break;
@@ -108,5 +118,27 @@ int main(void)
         free(rel);
     }
     oracle_graph_free(g);
+    /* line counts with a cached set over the per-query staging budget: a
+       2p query whose first hop has nf entries (1,024 staged, 1,025 not) */
+    for (int nf = 1024; nf <= 1025; nf++) {
+        const int64_t nh = nf + 3;
+        int32_t *ht = malloc((size_t)nh * 12);
+        for (int i = 0; i < nf; i++) { ht[3 * i] = 0; ht[3 * i + 1] = 0; ht[3 * i + 2] = 1 + i; }
+        const int32_t extra[3][3] = {{3, 1, 1150}, {1105, 1, 1151}, {1110, 1, 1151}};
+        for (int i = 0; i < 3; i++)
+            for (int k = 0; k < 3; k++) ht[3 * (nf + i) + k] = extra[i][k];
+        okg *h = oracle_graph_build(ht, nh, 1200, 2, 0, 2);
+        free(ht);
+        if (!h) return 8;
+        const int t2p = oracle_type_id("2p");
+        const int32_t ha[3] = {0, -1, -1}, hr[3] = {0, 1, -1};
+        for (uint32_t cut = 1; cut < 8; cut++) {
+            int64_t l64[3];
+            if (oracle_verify_lines(h, t2p, ha, hr, cut, 3, 0, 4000, l64)) continue;
+            const int32_t l32[3] = {(int32_t)l64[0], (int32_t)l64[1], (int32_t)l64[2]};
+            put("hublines", "2p", nf * 16 + (int)cut, l32, 3);
+        }
+        oracle_graph_free(h);
+    }
     return 0;
 }

@@ -5,8 +5,9 @@
   calls every entry point on a small random graph for all fourteen shapes:
   sampling with and without negatives, an exhausted draw budget, max_fanout,
   shared-candidate minibatches with an empty and a non-empty set,
-  verification with no candidates and with out-of-range ones, answer sets
-  and the bidirectional check on every node cut.  Each printed array must
+  verification with no candidates and with out-of-range ones, answer sets,
+  the bidirectional check and its line count on every node cut, and the
+  line count of a query whose cached set crosses the staging budget.  Each printed array must
   equal what the ordinary oracle build returns through its wrapper.
 * The sampling library's host side (the C ABI in capi.cpp) is compiled with
   the address sanitizer on the host pass only and linked with the library's
@@ -93,7 +94,24 @@ def test_oracle_under_sanitizers(tmp_path):
             member = np.isin(np.arange(V), as_i32(ans)).astype(np.int64)
             for cut in cuts:   # the bidirectional test is membership, on every node cut
                 assert np.array_equal(got[("bidir", qt, cut)], member), (qt, cut)
-                n_checked += 1
+                lb = got[("lines", qt, cut)]
+                assert lb[0] == b
+                want = g.verify_lines(qt, anc[b:b + 1], rel[b:b + 1], ref["positive"][b:b + 1],
+                                      cut, 5, b, 40)
+                assert np.array_equal(lb[1:], np.asarray(want).reshape(-1)), (qt, cut)
+                n_checked += 2
+    # a cached set just under and just over the staging budget
+    for nf in (1024, 1025):
+        ht = [[0, 0, 1 + i] for i in range(nf)] + [[3, 1, 1150], [1105, 1, 1151], [1110, 1, 1151]]
+        h = oracle.Graph(np.array(ht, np.int32), 1200, 2)
+        keys = [k for k in got if k[0] == "hublines" and k[2] // 16 == nf]
+        assert keys, nf
+        for k in keys:
+            want = h.verify_lines("2p", np.array([[0, -1, -1]], np.int32),
+                                  np.array([[0, 1, -1]], np.int32), np.array([1150], np.int32),
+                                  k[2] % 16, 3, 0, 4000)
+            assert np.array_equal(got[k], np.asarray(want).reshape(-1)), k
+            n_checked += 1
     assert n_checked > 500
 
 
