@@ -193,8 +193,8 @@ int smore_sample(const smore_graph *g, const smore_query_dag *dag, const smore_s
    contents, and each call initialises whatever it reads.  Errors as for
    smore_sample, and SMORE_E_UNSUPPORTED when the arguments need more
    scratch than the fixed size (smore_sample_workspace_bytes gives the
-   need; about 23 KB per query at 512 negatives and 2,048 draws, e.g.
-   2,048 such queries, or 16,384 queries with 64 negatives and 256
+   need; about 15 KB per query at 512 negatives and 2,048 draws, e.g.
+   4,096 such queries, or 16,384 queries with 64 negatives and 256
    draws). */
 #define SMORE_NOALLOC_SCRATCH_BYTES (64u << 20)
 int smore_sample_noalloc(const smore_graph *g, const smore_query_dag *dag,

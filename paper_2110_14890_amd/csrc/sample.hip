@@ -656,7 +656,6 @@ struct Ws {
     int32_t* ctrl;    // [0] queue pushes [1] queue pops [2 + k] size of active list k
                       // [5] 3p units pushed
     int32_t* qf;      // [B][QF]: list k at [2k, 2k+1) edge range; [6] bit k: list k staged
-    int32_t* cval;    // [B][neg_tries] candidate ids
     uint8_t* status;  // [B][neg_tries] ST_*
     int32_t* act[2];  // active query lists
     int2* queue;      // (query, draw) items
@@ -666,6 +665,22 @@ struct Ws {
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Candidate j of query b: draw j of the query's own stream, pick(U(NEG, q,
+// 0, j), V) with q = query_offset + b (Sec. 3.2: candidates uniform over the
+// entities), or entry j of the caller's list or the shared set, -1 when it
+// is not an entity.  Every kernel that needs a candidate takes it from here,
+// so the draws are recomputed where they are used instead of being stored
+// and read back.
+__device__ __forceinline__ int32_t candidate(const SampleParams& p, int32_t V, int32_t b, int32_t j)
+{
+    if (p.shared_mode != 0) {
+        const int32_t c = p.shared[(int64_t)p.cand_stride * b + j];
+        return (uint32_t)c >= (uint32_t)V ? -1 : c;
+    }
+    const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
+    return (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)V);
+}
 
 // Round r covers draws [round_end(r-1), round_end(r)): first n_neg plus a
 // small margin (a query rarely rejects more than a few percent of its
@@ -707,7 +722,6 @@ size_t ws_layout(const SampleParams& p, Ws* w, char* base)
     Ws x;
     x.ctrl = (int32_t*)take(64 * sizeof(int32_t));
     x.qf = (int32_t*)take((size_t)B * QF * sizeof(int32_t));
-    x.cval = (int32_t*)take((size_t)B * T * sizeof(int32_t));
     x.status = (uint8_t*)take((size_t)B * T);
     x.act[0] = (int32_t*)take((size_t)B * sizeof(int32_t));
     x.act[1] = (int32_t*)take((size_t)B * sizeof(int32_t));
@@ -1127,7 +1141,6 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
     for (int32_t qi = uni(blockIdx.x * (CWG / 64) + w); qi < nact; qi += nwaves) {
         // the first round lists every query in order: the list is not read
         const int32_t b = j0 == 0 ? qi : uni(ws.act[cur][qi]);
-        const uint32_t q = (uint32_t)(p.query_offset + (uint64_t)b);
         int32_t anc[3], rel[3];
         for (int k = 0; k < 3; ++k) {
             anc[k] = uni(out.anchors[3 * (int64_t)b + k]);
@@ -1161,7 +1174,6 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             }
             wave_sync();
         };
-        int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         // first test of every draw: the staged root-edge lists when the
         // shape has them (LDS only), else the in-edge mask; in the latter
@@ -1198,13 +1210,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 c[k] = 0;
                 word[k] = 0;
                 if (j < j1) {
-                    if constexpr (SH) {
-                        c[k] = p.shared[(int64_t)p.cand_stride * b + j];
-                        if ((uint32_t)c[k] >= (uint32_t)g.V) c[k] = -1;   // never a negative
-                    } else {
-                        c[k] = (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j),
-                                                     (uint32_t)g.V);
-                    }
+                    c[k] = candidate(p, g.V, b, j);   // -1 (given candidates only): never a negative
                     if (!use_lists && c[k] >= 0)
                         word[k] = two_level ? g.has_in4[c[k] >> 7] : g.has_in[c[k] >> 5];
                 }
@@ -1247,7 +1253,6 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 const bool in = live && c[k] >= 0 && ((word[k] >> (c[k] & 31)) & 1u);
                 if (live) {
                     if (!use_lists && !two_level && c[k] >= 0) tl.read(g.has_in + (c[k] >> 5), 4);
-                    cv[j] = c[k];
                     if (!in) sv[j] = c[k] >= 0 ? ST_NON : ST_DUP;   // ST_DUP: not an entity
                 }
                 const uint64_t m = __ballot(in);
@@ -1346,7 +1351,7 @@ __global__ __launch_bounds__(HEAVY_WG) void k_heavy(GraphView g, SampleParams p,
             const int2 it = ws.queue[mine];
             mb = it.x;
             mat = (int64_t)it.x * p.neg_tries + it.y;
-            mc = ws.cval[mat];
+            mc = candidate(p, g.V, it.x, it.y);
 #pragma unroll
             for (int k = 0; k < 3; ++k) mrel[k] = out.relations[3 * (int64_t)mb + k];
             const int32_t* qb = ws.qf + (int64_t)mb * QF;
@@ -1571,7 +1576,7 @@ __device__ __forceinline__ Slice3 item_slice3(const GraphView& g, const SamplePa
     w.valid = true;
     w.b = it.x;
     w.mat = (int64_t)it.x * p.neg_tries + it.y;
-    const int32_t c = ws.cval[w.mat];
+    const int32_t c = candidate(p, g.V, it.x, it.y);
     w.r1 = out.relations[3 * (int64_t)w.b + 1];
     const int32_t r2 = out.relations[3 * (int64_t)w.b + 2];
     const int32_t* qb = ws.qf + (int64_t)w.b * QF;
@@ -1679,8 +1684,9 @@ __device__ __forceinline__ int32_t ht_first(const int32_t* tv, const int32_t* tj
 // states): keep draw j iff it is not an answer and no earlier draw has the
 // same value; the first n_neg kept, in draw order, are the negatives.
 // Queries neither complete nor out of budget go to the next round's list.
-__global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out out, Ws ws, int cur,
-                                                int32_t j_end, int last, int32_t tcap, int tshift)
+__global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore_sample_out out, Ws ws,
+                                                int cur, int32_t j_end, int last, int32_t tcap,
+                                                int tshift)
 {
     extern __shared__ int32_t lds[];
     int32_t* tv = lds;
@@ -1696,12 +1702,11 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, smore_sample_out
     for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
         const int32_t b = uni(ws.act[cur][qi]);
         if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
-        const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
         for (int32_t k = lane; k < tcap; k += 64) { tv[k] = -1; tj[k] = INT_MAX; }
         for (int32_t j = lane; j < j_end; j += 64) {
-            vals[j] = cv[j];
+            vals[j] = candidate(p, V, b, j);
             sts[j] = sv[j];
         }
         wave_sync();
@@ -1751,9 +1756,10 @@ constexpr int CWAVES = 4;
 // itself is not read then, and the query's validity flag is loaded beside
 // the draws rather than before them).
 template <int NK>
-__global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smore_sample_out out,
-                                                             Ws ws, int cur, int32_t j_end, int last,
-                                                             int32_t tcap, int tshift, int ident)
+__global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int32_t V,
+                                                             smore_sample_out out, Ws ws, int cur,
+                                                             int32_t j_end, int last, int32_t tcap,
+                                                             int tshift, int ident)
 {
     extern __shared__ int32_t lds[];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -1766,7 +1772,6 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
     for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
         const int32_t b = ident ? qi : uni(ws.act[cur][qi]);
         const int32_t flag = ws.qf[(int64_t)b * QF + 6];   // < 0: query without a valid positive
-        const int32_t* cv = ws.cval + (int64_t)b * p.neg_tries;
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
         int32_t c[NK];
@@ -1776,10 +1781,13 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, smo
             const int32_t j = 64 * k + lane;
             c[k] = -1;
             st[k] = ST_ANS;
-            if (k < nk && j < j_end) {
-                c[k] = cv[j];
-                st[k] = sv[j];
-            }
+            if (k < nk && j < j_end) st[k] = sv[j];
+        }
+        // the draws themselves are recomputed while the states are in flight
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            const int32_t j = 64 * k + lane;
+            if (k < nk && j < j_end) c[k] = candidate(p, V, b, j);
         }
         if (uni(flag) < 0) continue;
         bool non[NK];
@@ -1954,10 +1962,10 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             prof_mark(2, r, false, st);
             const size_t tab = (size_t)CWAVES * tcap * sizeof(int32_t);
             if (j_end <= 64 * 9)
-                k_compact_reg<9><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                k_compact_reg<9><<<grid, 64 * CWAVES, tab, st>>>(p, gv.V, out, ws, cur, j_end,
                                                                  r == rounds - 1, tcap, tshift, r == 0);
             else
-                k_compact_reg<CK><<<grid, 64 * CWAVES, tab, st>>>(p, out, ws, cur, j_end,
+                k_compact_reg<CK><<<grid, 64 * CWAVES, tab, st>>>(p, gv.V, out, ws, cur, j_end,
                                                                   r == rounds - 1, tcap, tshift, r == 0);
             if ((rc = check_launch(err))) return rc;
             prof_mark(2, r, true, st);
@@ -1976,8 +1984,8 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             attr = true;
         }
         prof_mark(2, r, false, st);
-        k_compact<<<grid * 4, 64, lds, st>>>(p, out, ws, cur, j_end, r == rounds - 1, tcap,
-                                                       tshift);
+        k_compact<<<grid * 4, 64, lds, st>>>(p, gv.V, out, ws, cur, j_end, r == rounds - 1, tcap,
+                                             tshift);
         if ((rc = check_launch(err))) return rc;
         prof_mark(2, r, true, st);
     }
