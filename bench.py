@@ -346,10 +346,10 @@ GRAPH_BUILD_KERNELS = ("k_radix", "k_scan", "k_add", "k_flag", "k_write_g", "k_n
                        "k_load", "k_has_in", "k_compact_active", "k_sig")
 
 
-def profile_commands(config, steps):
+def profile_commands(config, steps, root):
     cfgflag = "" if config == "freebase" else f" --config {config}"
     run = f"python3 -u bench.py{cfgflag} --no-cpu-baseline --no-gather-ceiling --no-oracle-lines"
-    d = f"gpurun_out/prof_{config}"
+    d = f"{root}/prof_{config}"
     return [
         f"mkdir -p {d}/trace",
         f"rocprofv3 --kernel-trace --stats -d {d}/trace -o bench --output-format csv -- {run} "
@@ -456,9 +456,9 @@ def summarize_profiles(config, folder, steps):
          "each step samples a new batch of query ids.\n",
          f"Profiled sources: `paper_2110_14890_amd/csrc/sample.hip` sha256 prefix `{sha}`.\n",
          "Commands (from the repository root after `cd /tmp && export TMPDIR=/tmp`, each a separate "
-         "process), then `python3 bench.py --summarize " + f"gpurun_out/prof_{config}"
+         "process), then `python3 bench.py --summarize " + folder.rstrip("/")
          + ("" if config == "freebase" else f" --config {config}") + "` to write this file:\n", "```"]
-    L += profile_commands(config, steps) + ["```\n"]
+    L += profile_commands(config, steps, os.path.dirname(os.path.normpath(folder)) or ".") + ["```\n"]
     L.append("Kernels are grouped by name and, for the candidate and long-list kernels, by round of "
              "candidate draws (round 0 covers the first n_neg + n_neg / 32 + 8 draws). "
              "\"accounting\" rows are the one untimed pass with the kernels' own read tally.\n")
@@ -583,13 +583,16 @@ def main():
                     help="only write the profiles/ summaries of --config from the rocprofv3 output "
                          "under DIR (see profile_commands)")
     ap.add_argument("--print-profile-commands", action="store_true",
-                    help="only print the rocprofv3 commands whose output --summarize reads")
+                    help="only print the rocprofv3 commands whose output --summarize reads "
+                         "(written under PROFILE_ROOT/prof_<config>)")
+    ap.add_argument("--profile-root", default="prof_runs",
+                    help="folder the printed rocprofv3 commands write under")
     args = ap.parse_args()
     args.concurrent = not (args.chained or args.serial or args.split)
     args.prepare_ahead = args.chained and not args.wait_before_prepare
 
     if args.print_profile_commands:
-        print("\n".join(profile_commands(args.config, args.steps)))
+        print("\n".join(profile_commands(args.config, args.steps, args.profile_root)))
         return
     if args.summarize:
         summarize_profiles(args.config, args.summarize, args.steps)
