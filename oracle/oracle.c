@@ -947,12 +947,15 @@ int oracle_bidir_check(const okg *g, int qtype, const int32_t *anchors, const in
    - a list met with a forward-cached set: the shorter side gives the keys
      in ascending order, each key is looked up in the other side by the
      same lower-bound search, up to the first common entity; list keys and
-     list probes are read; a cached set that fits the STAGE_BUDGET entries
-     staged per query (each cut set in node order is staged when it fits in
-     what the sets staged before it left of the budget) is held on chip, so its keys and probes are free,
-     while a larger one is searched where it is stored: the forward group
-     A_r(a) when the set is one projection of an anchor (the only kind the
-     strict cut caches), else a sorted array of its own;
+     list probes are read;
+   - an entity tested for membership in a forward-cached set: the same
+     lower-bound search of the set;
+   - a cached set that fits the STAGE_BUDGET entries staged per query (each
+     cut set in node order is staged when it fits in what the sets staged
+     before it left of the budget) is held on chip, so its keys and probes
+     are free, while a larger one is searched where it is stored: the
+     forward group A_r(a) when the set is one projection of an anchor (the
+     only kind the strict cut caches), else a sorted array of its own;
    - forward caching: every cut set once, from the anchors, with the same
      reads (node entries, group search, the whole list).
    The candidates of query qid are draws j < n_draws, c_j =
@@ -1078,7 +1081,21 @@ static int vmeet(vlines *L, int part, int64_t b, int64_t e, int k_set)
 
 static int vmember(vlines *L, int k, int32_t x, int part)
 {
-    if (L->cut & (1u << k)) return set_has(L->F[k], x);
+    if (L->cut & (1u << k)) {
+        const iset F = L->F[k];
+        if (L->staged[k]) return set_has(F, x);
+        /* a set over the staging budget: the same lower-bound search, where
+           it is stored */
+        int64_t lo = 0, hi = F.n;
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            vset_read(L, part, k, mid);
+            if (F.v[mid] < x) lo = mid + 1; else hi = mid;
+        }
+        if (lo == F.n) return 0;
+        vset_read(L, part, k, lo);
+        return F.v[lo] == x;
+    }
     const onode *nd = &L->T->nd[k];
     if (nd->op == N_ANCHOR) return x == L->anchors[nd->slot];
     if (nd->op == N_NOT) return !vmember(L, nd->ch[0], x, part);

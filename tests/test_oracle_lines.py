@@ -7,7 +7,8 @@ grp[S+1] int32 pairs, nbr[E] int32 per direction).
   of every read follow from those indices and the byte offsets 4v, 8s and
   4e, so each expected line set is derived without the oracle's code.
 * A cached set one entry over the per-query staging budget is searched
-  where it is stored (its forward group), one entry under it is free.
+  where it is stored (its forward group), one entry under it is free; so
+  is a membership test in it, and sets are staged greedily in node order.
 * Invariants on random graphs for all fourteen shapes: every draw reads its
   own node entries (a lower bound from the draws alone), the parts bound
   the total, a graph whose lists never exceed eight entries puts nothing in
@@ -155,6 +156,39 @@ def test_cached_set_over_the_staging_budget_is_searched_in_place(oracle_lib, n_f
         else:
             assert got[0].tolist() == [base + len(rnbr), 0, base + len(rnbr)], qid
     assert seen == {1150, 1151}
+
+
+def test_membership_in_a_set_over_the_budget_and_greedy_staging(oracle_lib):
+    # ip: F0 = A_r0(0) = {1..1025} (forward edges 0..1024) is over the
+    # budget; F1 = A_r1(2000) = {3, 5} (forward edges 1027, 1028: heads 3 and
+    # 4 hold edges 1025, 1026 under r2) still fits what F0 left, so it is
+    # staged (greedy in node order).  The only in-edges under r2 end at
+    # 3000, from 3 and 4 (reverse edges 1027, 1028: tails 1..1025 hold edges
+    # 0..1026, tails 3 and 5 two each).  Verifying 3000 expands its list in
+    # the long part: entry 3 (edge 1027, reverse line 64) is tested in F0 by
+    # bisection in its forward group - probes 512, 256, ..., 2, 1 and a last
+    # read of entry 2, lines 32, 16, 8, 4, 2, 1, 0 - and in F1 for free, and
+    # it is in both, so 3 decides.  The forward lines are part 0's as well
+    # (forward caching reads F0 whole), so the total grows by one line.
+    V = 3100
+    tr = ([[0, 0, y] for y in range(1, 1026)] + [[2000, 1, 3], [2000, 1, 5]]
+          + [[3, 2, 3000], [4, 2, 3000]])
+    g = oracle_lib.Graph(np.array(tr, np.int32), V, 3)
+    anchors = np.array([[0, 2000, -1]], np.int32)
+    rels = np.array([[0, 1, 2]], np.int32)
+    assert sorted(np.asarray(g.answer_set("ip", anchors[0], rels[0])).tolist()) == [3000]
+    pos = np.array([3000], np.int32)
+    n, seed = 2000, 4
+    seen = {True: 0, False: 0}
+    for qid in range(12):
+        drawn = 3000 in draws(oracle_lib, seed, qid, n, V)
+        got = g.verify_lines("ip", anchors, rels, pos, strict_mask(oracle_lib, "ip"), seed, qid, n)[0]
+        if drawn:
+            assert got[1] == 8 and got[2] == got[0] + 1, (qid, got)
+        else:
+            assert got[1] == 0 and got[2] == got[0], (qid, got)
+        seen[drawn] += 1
+    assert seen[True] and seen[False]
 
 
 @pytest.mark.parametrize("qt", ["1p", "2p", "3p", "2i", "3i", "ip", "pi", "2u", "up",
