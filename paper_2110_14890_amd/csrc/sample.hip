@@ -684,33 +684,51 @@ __device__ __forceinline__ int32_t candidate(const SampleParams& p, int32_t V, i
     return (int32_t)reduce_range(draw64(p.seed, TAG_NEG, q, 0, (uint32_t)j), (uint32_t)V);
 }
 
-// Round r covers draws [round_end(r-1), round_end(r)): first n_neg plus a
-// small margin (a query rarely rejects more than a few percent of its
-// draws), then four times as many, up to neg_tries.
-inline int32_t round_end(const SampleParams& p, int r)
+// Rounds of candidate draws.  Round 0 takes draws [0, first_round(p)) of
+// every query: n_neg plus a small margin (a query rarely rejects more than
+// a few percent of its draws).  A query still short of n_neg after a round
+// takes its own next range: the draws its deficit needs at the acceptance
+// rate it has had so far, with a margin (next_round_end); the last round
+// takes every query still short to neg_tries.  Rounds are a scheduling
+// detail: a query's negatives are its first n_neg accepted draws in draw
+// order whatever the rounds were.
+inline int32_t first_round(const SampleParams& p)
 {
-    int64_t e = p.n_neg + p.n_neg / 32 + 8;
-    for (int k = 0; k < r; ++k) e *= 4;
+    const int64_t e = (int64_t)p.n_neg + p.n_neg / 32 + 8;
     return (int32_t)(e < p.neg_tries ? e : p.neg_tries);
 }
 
 inline int n_rounds(const SampleParams& p)
 {
-    int r = 0;
-    while (round_end(p, r) < p.neg_tries) ++r;
-    return r + 1;
+    return first_round(p) < p.neg_tries ? 3 : 1;
 }
 
+// Longest range one query takes in one round.
 inline int32_t max_round_len(const SampleParams& p)
 {
-    int32_t m = 0, prev = 0;
-    for (int r = 0; r < n_rounds(p); ++r) {
-        const int32_t e = round_end(p, r);
-        m = e - prev > m ? e - prev : m;
-        prev = e;
-    }
-    return m;
+    const int32_t e0 = first_round(p);
+    return e0 > p.neg_tries - e0 ? e0 : p.neg_tries - e0;
 }
+
+// End of the next range of a query that has `kept` accepted draws among its
+// first `end`: the deficit over that acceptance rate, a quarter more, and
+// 16 draws; everything up to neg_tries when nothing was accepted yet or the
+// next round is the last.
+__device__ __forceinline__ int32_t next_round_end(const SampleParams& p, int32_t end, int32_t kept,
+                                                  bool to_last)
+{
+    if (to_last || kept <= 0) return p.neg_tries;
+    const int64_t need = (int64_t)(p.n_neg - kept) * end;
+    const int64_t more = (need * 5 + 4 * (int64_t)kept - 1) / (4 * (int64_t)kept) + 16;
+    return (int32_t)(end + more < p.neg_tries ? end + more : p.neg_tries);
+}
+
+// A query's draw range of a later round, kept in its per-query block (two
+// 16-bit draw indices).
+static_assert(SMORE_MAX_NEG_TRIES < 65536, "draw indices must fit 16 bits");
+__host__ __device__ __forceinline__ int32_t pack_range(int32_t a, int32_t b) { return a | (b << 16); }
+__host__ __device__ __forceinline__ int32_t range_lo(int32_t r) { return r & 0xFFFF; }
+__host__ __device__ __forceinline__ int32_t range_hi(int32_t r) { return (int32_t)((uint32_t)r >> 16); }
 
 size_t ws_layout(const SampleParams& p, Ws* w, char* base)
 {
@@ -1151,6 +1169,14 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
         const int32_t* qb = ws.qf + (int64_t)b * QF;
         const int32_t staged = uni(qb[6]);
         if (staged < 0) continue;   // query without a valid positive
+        // this round's draws: [j0, j1) in the first round, else the query's
+        // own range, set by the previous round's selection
+        int32_t qj0 = j0, qj1 = j1;
+        if (j0 < 0) {
+            const int32_t rg = uni(qb[7]);
+            qj0 = range_lo(rg);
+            qj1 = range_hi(rg);
+        }
         FSet F[3];
         int32_t sbeg[3], used = 0;
 #pragma unroll
@@ -1193,7 +1219,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
             stage_lists();
             to_stage = false;
         }
-        for (int32_t base = j0; base < j1; base += WIN) {
+        for (int32_t base = qj0; base < qj1; base += WIN) {
             // Every answer of every shape is reached by a projection, so a
             // draw without an in-edge is a non-answer: the in-edge mask (V
             // bits, resident in the last-level cache) decides most draws.
@@ -1211,7 +1237,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
                 const int32_t j = base + k * 64 + lane;
                 c[k] = 0;
                 word[k] = 0;
-                if (j < j1) {
+                if (j < qj1) {
                     c[k] = candidate(p, g.V, b, j);   // -1 (given candidates only): never a negative
                     if (!use_lists && c[k] >= 0)
                         word[k] = two_level ? g.has_in4[c[k] >> 7] : g.has_in[c[k] >> 5];
@@ -1225,7 +1251,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
 #pragma unroll
                 for (int k = 0; k < DPW; ++k) {
                     // accounted as one mask line per draw, as the one-level test
-                    const bool live = base + k * 64 + lane < j1 && c[k] >= 0;
+                    const bool live = base + k * 64 + lane < qj1 && c[k] >= 0;
                     const bool maybe = live && ((word[k] >> ((c[k] >> 2) & 31)) & 1u);
                     if (live) tl.read(g.has_in4 + (c[k] >> 7), 4);
                     const uint32_t sg = maybe ? (uint32_t)g.sig[c[k]] : 0u;
@@ -1251,7 +1277,7 @@ __global__ __launch_bounds__(CWG) void k_candidates(GraphView g, SampleParams p,
 #pragma unroll
             for (int k = 0; k < DPW; ++k) {
                 const int32_t j = base + k * 64 + lane;
-                const bool live = j < j1;
+                const bool live = j < qj1;
                 const bool in = live && c[k] >= 0 && ((word[k] >> (c[k] & 31)) & 1u);
                 if (live) {
                     if (!use_lists && !two_level && c[k] >= 0) tl.read(g.has_in + (c[k] >> 5), 4);
@@ -1687,8 +1713,8 @@ __device__ __forceinline__ int32_t ht_first(const int32_t* tv, const int32_t* tj
 // same value; the first n_neg kept, in draw order, are the negatives.
 // Queries neither complete nor out of budget go to the next round's list.
 __global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore_sample_out out, Ws ws,
-                                                int cur, int32_t j_end, int last, int32_t tcap,
-                                                int tshift)
+                                                int cur, int32_t j_end, int last, int next_last,
+                                                int32_t tcap, int tshift, int ident)
 {
     extern __shared__ int32_t lds[];
     int32_t* tv = lds;
@@ -1704,22 +1730,24 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore
     for (int32_t qi = blockIdx.x; qi < nact; qi += gridDim.x) {
         const int32_t b = uni(ws.act[cur][qi]);
         if (uni(ws.qf[(int64_t)b * QF + 6]) < 0) continue;   // query without a valid positive
+        // the query's draws so far (at most j_end, which sizes the LDS)
+        const int32_t jq = ident ? j_end : range_hi(uni(ws.qf[(int64_t)b * QF + 7]));
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
         for (int32_t k = lane; k < tcap; k += 64) { tv[k] = -1; tj[k] = INT_MAX; }
-        for (int32_t j = lane; j < j_end; j += 64) {
+        for (int32_t j = lane; j < jq; j += 64) {
             vals[j] = candidate(p, V, b, j);
             sts[j] = sv[j];
         }
         wave_sync();
-        for (int32_t j = lane; j < j_end; j += 64) ht_insert(tv, tj, tmask, tshift, vals[j], j);
+        for (int32_t j = lane; j < jq; j += 64) ht_insert(tv, tj, tmask, tshift, vals[j], j);
         wave_sync();
         int32_t acc = 0;
-        for (int32_t row0 = 0; row0 < j_end && acc < p.n_neg; row0 += 64) {
+        for (int32_t row0 = 0; row0 < jq && acc < p.n_neg; row0 += 64) {
             const int32_t j = row0 + lane;
             int32_t c = 0;
             bool keep = false;
-            if (j < j_end) {
+            if (j < jq) {
                 c = vals[j];
                 keep = sts[j] == ST_NON && ht_first(tv, tj, tmask, tshift, c) == j;
             }
@@ -1731,13 +1759,14 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore
             }
             acc = uni(min(p.n_neg, acc + __popcll(m)));
         }
-        if (acc == p.n_neg || last) {
+        if (acc == p.n_neg || last || jq >= p.neg_tries) {
             for (int32_t k = acc + lane; k < p.n_neg; k += 64) row[k] = -1;
             if (lane == 0) {
                 out.n_valid[b] = acc;
                 if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
             }
         } else if (lane == 0) {
+            ws.qf[(int64_t)b * QF + 7] = pack_range(jq, next_round_end(p, jq, acc, next_last));
             ws.act[cur ^ 1][atomicAdd(&ws.ctrl[2 + (cur ^ 1)], 1)] = b;
         }
         wave_sync();
@@ -1760,8 +1789,8 @@ constexpr int CWAVES = 4;
 template <int NK>
 __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int32_t V,
                                                              smore_sample_out out, Ws ws, int cur,
-                                                             int32_t j_end, int last, int32_t tcap,
-                                                             int tshift, int ident)
+                                                             int32_t j_end, int last, int next_last,
+                                                             int32_t tcap, int tshift, int ident)
 {
     extern __shared__ int32_t lds[];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -1770,10 +1799,13 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int
     const uint32_t tmask = (uint32_t)tcap - 1;
     const int32_t nact = uni(ws.ctrl[2 + cur]);
     if (blockIdx.x == 0 && threadIdx.x == 0) { ws.ctrl[0] = 0; ws.ctrl[1] = 0; ws.ctrl[5] = 0; }
-    const int32_t nk = uni((j_end + 63) >> 6);
     for (int32_t qi = uni(blockIdx.x * CWAVES + w); qi < nact; qi += gridDim.x * CWAVES) {
         const int32_t b = ident ? qi : uni(ws.act[cur][qi]);
         const int32_t flag = ws.qf[(int64_t)b * QF + 6];   // < 0: query without a valid positive
+        // the query's draws so far: all of the first round, or up to the end
+        // of its own range in a later one
+        const int32_t jq = ident ? j_end : range_hi(uni(ws.qf[(int64_t)b * QF + 7]));
+        const int32_t nk = uni((jq + 63) >> 6);
         const uint8_t* sv = ws.status + (int64_t)b * p.neg_tries;
         int32_t* row = out.negatives + (int64_t)b * p.n_neg;
         int32_t c[NK];
@@ -1783,13 +1815,13 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int
             const int32_t j = 64 * k + lane;
             c[k] = -1;
             st[k] = ST_ANS;
-            if (k < nk && j < j_end) st[k] = sv[j];
+            if (k < nk && j < jq) st[k] = sv[j];
         }
         // the draws themselves are recomputed while the states are in flight
 #pragma unroll
         for (int k = 0; k < NK; ++k) {
             const int32_t j = 64 * k + lane;
-            if (k < nk && j < j_end) c[k] = candidate(p, V, b, j);
+            if (k < nk && j < jq) c[k] = candidate(p, V, b, j);
         }
         if (uni(flag) < 0) continue;
         bool non[NK];
@@ -1855,13 +1887,14 @@ __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int
             }
             acc = uni(min(p.n_neg, acc + __popcll(m)));
         }
-        if (acc == p.n_neg || last) {
+        if (acc == p.n_neg || last || jq >= p.neg_tries) {
             for (int32_t k = acc + lane; k < p.n_neg; k += 64) row[k] = -1;
             if (lane == 0) {
                 out.n_valid[b] = acc;
                 if (acc < p.n_neg) out.neg_draws[b] = p.neg_tries;
             }
         } else if (lane == 0) {
+            ws.qf[(int64_t)b * QF + 7] = pack_range(jq, next_round_end(p, jq, acc, next_last));
             ws.act[cur ^ 1][atomicAdd(&ws.ctrl[2 + (cur ^ 1)], 1)] = b;
         }
         wave_sync();   // the next query clears the table
@@ -1928,8 +1961,10 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
     const int rounds = n_rounds(p);
     for (int r = 0; r < rounds; ++r) {
         const int cur = r & 1;
-        const int32_t prev = r == 0 ? 0 : round_end(p, r - 1);   // the round's first draw
-        const int32_t j_end = round_end(p, r);
+        // the first round's draws are the same for every query; a later
+        // round's are each query's own (j0 = -1), ending at most at neg_tries
+        const int32_t j0 = r == 0 ? 0 : -1;
+        const int32_t j_end = r == 0 ? first_round(p) : p.neg_tries;
         // later rounds carry the few queries short of n_neg: a smaller grid
         // keeps their (often empty) launches cheap
         const int grid = r == 0 ? PERSIST_BLOCKS : PERSIST_BLOCKS / 4;
@@ -1941,7 +1976,7 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
                 if (e != hipSuccess) { *err = hipGetErrorString(e); return SMORE_E_HIP; }
             }
             prof_mark(0, r, false, st);
-            k_candidates<QT, T><<<cgrid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, prev, j_end);
+            k_candidates<QT, T><<<cgrid, CWG, 0, st>>>(gv, p, out, ws, stats, cur, j0, j_end);
             if ((rc = check_launch(err))) return rc;
             prof_mark(0, r, true, st);
         }
@@ -1965,10 +2000,12 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             const size_t tab = (size_t)CWAVES * tcap * sizeof(int32_t);
             if (j_end <= 64 * 9)
                 k_compact_reg<9><<<grid, 64 * CWAVES, tab, st>>>(p, gv.V, out, ws, cur, j_end,
-                                                                 r == rounds - 1, tcap, tshift, r == 0);
+                                                                 r == rounds - 1, r + 1 == rounds - 1,
+                                                                 tcap, tshift, r == 0);
             else
                 k_compact_reg<CK><<<grid, 64 * CWAVES, tab, st>>>(p, gv.V, out, ws, cur, j_end,
-                                                                  r == rounds - 1, tcap, tshift, r == 0);
+                                                                  r == rounds - 1, r + 1 == rounds - 1,
+                                                                  tcap, tshift, r == 0);
             if ((rc = check_launch(err))) return rc;
             prof_mark(2, r, true, st);
             continue;
@@ -1986,8 +2023,8 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
             attr = true;
         }
         prof_mark(2, r, false, st);
-        k_compact<<<grid * 4, 64, lds, st>>>(p, gv.V, out, ws, cur, j_end, r == rounds - 1, tcap,
-                                             tshift);
+        k_compact<<<grid * 4, 64, lds, st>>>(p, gv.V, out, ws, cur, j_end, r == rounds - 1,
+                                             r + 1 == rounds - 1, tcap, tshift, r == 0);
         if ((rc = check_launch(err))) return rc;
         prof_mark(2, r, true, st);
     }
