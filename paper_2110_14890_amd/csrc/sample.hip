@@ -698,9 +698,13 @@ inline int32_t first_round(const SampleParams& p)
     return (int32_t)(e < p.neg_tries ? e : p.neg_tries);
 }
 
+// Three rounds (first, own ranges, the rest); a batch under 4,096 queries
+// is bound by launches rather than draws, and its second round takes the
+// rest of the budget at once.
 inline int n_rounds(const SampleParams& p)
 {
-    return first_round(p) < p.neg_tries ? 3 : 1;
+    if (first_round(p) >= p.neg_tries) return 1;
+    return p.batch >= 4096 ? 3 : 2;
 }
 
 // Longest range one query takes in one round.
