@@ -268,6 +268,7 @@ void compile_walk(const smore_query_dag* d, int v, int reg, smore::WalkProgram* 
             const smore_dag_node &xa = d->node[x.child[0]], &ya = d->node[y.child[0]];
             if (xa.op != SMORE_OP_ANCHOR || ya.op != SMORE_OP_ANCHOR) continue;
             const int p = w->n_pairs++;
+            if (reg == 0) ++w->root_pairs;
             w->pair_anchor[p][0] = xa.slot;
             w->pair_anchor[p][1] = ya.slot;
             w->pair_rel[p][0] = x.slot;

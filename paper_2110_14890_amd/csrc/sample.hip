@@ -2,9 +2,9 @@
 //
 // Positives (smore_sample_positives), one kernel:
 //
-//  k_positive: PA lanes per query (two, or four for plans with a
-//    complemented operand), lane l running attempts l, l + PA, ...; the
-//    lowest successful attempt wins.
+//  k_positive: PA lanes per query (two; four or eight for plans that
+//    accept less often per attempt), lane l running attempts l, l + PA, ...;
+//    the lowest successful attempt wins.
 //    Reverse directional sampling
 //    (Sec. 3.1; appendix on reverse directional sampling): attempt t grounds
 //    the root among entities with an in-edge, then runs the pre-order walk
@@ -2282,12 +2282,15 @@ int launch_positive(const smore_graph* g, const WalkProgram& wp, const SamplePar
 {
     // attempt lanes per query (they divide 64): attempts past the first
     // successful one are wasted reads, so plans that usually succeed at once
-    // run two; plans with a complemented operand accept less often per
-    // attempt and run four
-    const int pa = wp.neg_steps > 0 ? 4 : 2;
+    // run two.  Plans accept less often per attempt when sibling branches
+    // hang off the root (two of them must not draw the same in-relation and
+    // in-neighbour of the root, which seldom has many) or with a
+    // complemented operand: four lanes, eight with three root siblings.
+    const int pa = wp.root_pairs >= 3 ? 8 : (wp.root_pairs > 0 || wp.neg_steps > 0) ? 4 : 2;
     const int64_t threads = (int64_t)p.batch * pa;
     const unsigned blocks = (unsigned)((threads + 255) / 256);
-    if (pa == 4) k_positive<4><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
+    if (pa == 8) k_positive<8><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
+    else if (pa == 4) k_positive<4><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
     else k_positive<2><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
     return check_launch(err);
 }

@@ -60,6 +60,7 @@ struct WalkProgram {
     int32_t pair_rel[3][2];
     int32_t neg_steps, neg_first, sib_step, neg_target, neg_anchor;
     int32_t neg_rel[2];
+    int32_t root_pairs;   // of the pairs, those whose siblings hang off the root entity
 };
 
 // Query shapes with a dedicated verification kernel: the nine without
