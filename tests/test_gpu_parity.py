@@ -123,6 +123,27 @@ def test_budget_exhaustion_and_small_graphs(qt):
         assert_same(got, ref, what=f"{qt} n_neg {n_neg} neg_tries {nt} pos_tries {pt}")
 
 
+@pytest.mark.parametrize("qt", ["1p", "2p", "3p", "3i", "ip", "2u", "pni"])
+def test_later_rounds_take_per_query_ranges(qt):
+    # a batch of 4,096 queries runs three rounds: the first n_neg + n_neg/32 + 8
+    # draws, then each short query's own range, then the rest of the budget.
+    # On a graph of 60 entities many candidates are answers or repeats, so
+    # queries end in every round and some exhaust the budget.
+    rng = np.random.default_rng(12)
+    tr = kgsynth.random_tiny(rng, 60, 2, 700)
+    g, og = graph_pair(tr, 60, 2, False)
+    ended_later = exhausted = 0
+    for n_neg, nt in [(24, 96), (24, 4096), (40, 60)]:
+        got = gpu_sample(g, qt, 4096, n_neg, seed=5, neg_tries=nt)
+        ref = og.sample(qt, 4096, n_neg, seed=5, neg_tries=nt)
+        assert_same(got, ref, what=f"{qt} n_neg {n_neg} neg_tries {nt}")
+        first = min(n_neg + n_neg // 32 + 8, nt)
+        ok = got["n_valid"] == n_neg
+        ended_later += int((ok & (got["neg_draws"] > first)).sum())
+        exhausted += int(((got["n_valid"] >= 0) & ~ok).sum())
+    assert ended_later > 0 and exhausted > 0
+
+
 @pytest.mark.parametrize("qt", ["1p", "2p", "3p", "ip", "pi", "up", "inp", "pin", "pni"])
 def test_max_fanout(qt):
     cfg, tr = config_graph("fb15k237")
