@@ -2285,8 +2285,11 @@ int launch_positive(const smore_graph* g, const WalkProgram& wp, const SamplePar
     // run two.  Plans accept less often per attempt when sibling branches
     // hang off the root (two of them must not draw the same in-relation and
     // in-neighbour of the root, which seldom has many) or with a
-    // complemented operand: four lanes, eight with three root siblings.
-    const int pa = wp.root_pairs >= 3 ? 8 : (wp.root_pairs > 0 || wp.neg_steps > 0) ? 4 : 2;
+    // complemented operand: four lanes, eight with three root siblings; and
+    // a maximum expansion C rejects every attempt through a wider step:
+    // eight lanes.
+    const int pa = (wp.root_pairs >= 3 || p.max_fanout > 0) ? 8
+                   : (wp.root_pairs > 0 || wp.neg_steps > 0) ? 4 : 2;
     const int64_t threads = (int64_t)p.batch * pa;
     const unsigned blocks = (unsigned)((threads + 255) / 256);
     if (pa == 8) k_positive<8><<<blocks, 256, 0, st>>>(view_of(g), wp, p, out);
