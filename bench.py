@@ -106,10 +106,11 @@ def workload_name(cfg, types):
 
 
 def traffic_for(config, kernel):
-    """HBM bytes per launch of `kernel` (e.g. "k_candidates<3p> r0") from the
-    committed rocprofv3 counter summary of the workload (FETCH_SIZE and
-    WRITE_SIZE scaled by a plain copy's readings), or None when there is
-    none or it was taken on other sources of the sampling kernels."""
+    """HBM bytes per launch of `kernel` (e.g. "k_candidates<3p> r0", or
+    kernels joined by " + ", summed) from the committed rocprofv3 counter
+    summary of the workload (FETCH_SIZE and WRITE_SIZE scaled by a plain
+    copy's readings), or None when there is none or it was taken on other
+    sources of the sampling kernels."""
     path = os.path.join(ROOT, "profiles", f"negatives_{config}_hbm_bytes.txt")
     if not os.path.exists(path):
         return None
@@ -126,7 +127,8 @@ def traffic_for(config, kernel):
                 fields[key.strip()] = val.strip()
     if fields.get("sample_hip_sha256_16") != sample_hip_sha():
         return None
-    return kernels.get(kernel)
+    parts = [kernels.get(k) for k in kernel.split(" + ")]
+    return None if any(x is None for x in parts) else sum(parts)
 
 
 def gather_ceiling(stream):
@@ -478,10 +480,13 @@ def summarize_profiles(config, folder, steps):
                  "the launch on its stream), average over the timed steps:\n")
         L += ["| kernel | events (ms) | trace avg (ms) |", "|---|---|---|"]
         for kr in bench_line.get("kernels", []):
-            base, rd = kr["kernel"].split(" r")
-            tr_ = dur.get((base, int(rd)))
+            avgs = []
+            for part in kr["kernel"].split(" + "):    # kernels timed as one unit: their sum
+                base, rd = part.rsplit(" r", 1)
+                tr_ = dur.get((base, int(rd)))
+                avgs.append(sum(tr_) / len(tr_) / 1e3 if tr_ else None)
             L.append("| %s | %.4f | %s |" % (kr["kernel"], kr["avg_launch_ms"],
-                                             "%.4f" % (sum(tr_) / len(tr_) / 1e3) if tr_ else "-"))
+                                             "-" if None in avgs else "%.4f" % sum(avgs)))
         L.append("")
     L += ["## HBM counters (KiB per dispatch, averaged over the launches of each group)\n",
           "Calibration: a plain device copy of 1 GiB reads %.1f KiB of FETCH_SIZE and %.1f KiB of "
@@ -892,7 +897,9 @@ def main():
     def kernel_roofline(qt, kind):
         d = per_type[qt]
         ms = d["candidate_kernel_ms"] if kind == "cand" else d["long_list_kernel_ms"]
-        name = f"k_candidates<{qt}> r0" if kind == "cand" else f"k_heavy<{qt}> r0"
+        # the events around 3p's long-list work span its batched kernel and its unit kernel
+        name = (f"k_candidates<{qt}> r0" if kind == "cand" else
+                "k_heavy<3p> r0 + k_units<3p> r0" if qt == "3p" else f"k_heavy<{qt}> r0")
         tally = acct[qt]["cand_lines" if kind == "cand" else "heavy_lines"] * 64
         algo = None
         if lines:
