@@ -305,8 +305,9 @@ int smore_verify(const smore_graph *g, const smore_query_dag *dag, const smore_s
 /* Instrumentation: the next smore_sample or smore_sample_negatives call
    made by this thread records the caller's HIP events (hipEvent_t) on its
    stream immediately before and after one of its kernels in the first
-   round of candidate draws: which = 0 the candidate kernel, 1 the kernel
-   that intersects long lists, 2 the ordered selection.  Each `which` has
+   round of candidate draws: which = 0 the candidate kernel, 1 the kernels
+   that intersect long lists (for 3p the batched long-list kernel and the
+   kernel of its units, timed together), 2 the ordered selection.  Each `which` has
    its own arm, so one call can time several kernels.  One-shot: the
    next smore_sample, smore_sample_negatives or smore_sample_negatives_part
    call of this thread disarms all of them whether or not they recorded,
