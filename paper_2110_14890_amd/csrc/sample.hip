@@ -565,7 +565,8 @@ __global__ __launch_bounds__(256) void k_positive(GraphView g, WalkProgram wp, S
 //                 than 1,024 draws): first-occurrence test of every draw so
 //                 far, ordered selection of the first n_neg kept.
 // Queries still short of n_neg after a round go to the next round through a
-// device-side list, so rounds need no host synchronisation.
+// device-side list, each with the draw range the selection sets for it, so
+// rounds need no host synchronisation.
 
 // Lists per shape (anchor slot, relation slot) at the cut the planner picks:
 //   1p {a0}, 2p/3p {V1}, 2i/3i/2u/2in/3in {anchors}, ip/up/inp {Y0, Y1},
@@ -1715,7 +1716,8 @@ __device__ __forceinline__ int32_t ht_first(const int32_t* tv, const int32_t* tj
 // holds the round's first-occurrence table and the query's draws and
 // states): keep draw j iff it is not an answer and no earlier draw has the
 // same value; the first n_neg kept, in draw order, are the negatives.
-// Queries neither complete nor out of budget go to the next round's list.
+// Queries neither complete nor out of budget go to the next round's list
+// with their next draw range (next_round_end).
 __global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore_sample_out out, Ws ws,
                                                 int cur, int32_t j_end, int last, int next_last,
                                                 int32_t tcap, int tshift, int ident)
@@ -1786,10 +1788,10 @@ __global__ __launch_bounds__(64) void k_compact(SampleParams p, int32_t V, smore
 constexpr int CK = 16;
 constexpr int CWAVES = 4;
 
-// One wavefront per listed query; its draws and states are read in one
-// round trip (the first round lists every query in order, so the list
-// itself is not read then, and the query's validity flag is loaded beside
-// the draws rather than before them).
+// One wavefront per listed query; its states are read in one round trip
+// while its draws are recomputed (the first round lists every query in
+// order, so the list itself is not read then, and the query's validity flag
+// is loaded beside the states rather than before them).
 template <int NK>
 __global__ __launch_bounds__(64 * CWAVES) void k_compact_reg(SampleParams p, int32_t V,
                                                              smore_sample_out out, Ws ws, int cur,
