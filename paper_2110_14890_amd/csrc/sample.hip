@@ -1989,9 +1989,13 @@ int run_negatives(const GraphView& gv, const SampleParams& p, const smore_sample
         if (!(parts & NEG_REST)) continue;
         prof_mark(1, r, false, st);
         if constexpr (QT == Q3P) {
-            k_heavy3<T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
+            // a quarter grid in every round: these waves mostly wait on
+            // dependent reads, and at four waves per SIMD a full grid would
+            // hold the registers that the candidate kernels of shapes sampled
+            // beside this one need
+            k_heavy3<T><<<PERSIST_BLOCKS / 4, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
             if ((rc = check_launch(err))) return rc;
-            k_units3<T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats);
+            k_units3<T><<<PERSIST_BLOCKS / 4, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats);
         } else {
             k_heavy<QT, T><<<grid, HEAVY_WG, 0, st>>>(gv, p, out, ws, stats, cur ^ 1);
         }
