@@ -1,6 +1,7 @@
 """CPU checks of bench.py's measurement tooling: the HBM bytes it takes
 from the committed rocprofv3 summaries, the profiling commands it prints,
 and the CPU baseline's sampling on a small workload."""
+import dataclasses
 import re
 
 import pytest
@@ -47,12 +48,14 @@ def test_profile_commands(config):
 
 
 def test_cpu_baseline_times_a_small_workload_over_a_measurable_span():
-    cfg = kgsynth.CONFIGS["tiny"]
+    # a batch of 16 queries: the oracle finishes it within the time slice
+    # even on a loaded host, so the sample must go on past it
+    cfg = dataclasses.replace(kgsynth.CONFIGS["tiny"], batch=16)
     tr = kgsynth.generate(cfg, threads=2)
     og = oracle.Graph(tr, cfg.n_entities, cfg.n_relations, cfg.add_inverse, threads=2)
     r = bench.cpu_baseline(cfg, og, ["1p", "2p"], 0.6, 2, 2)
     assert r["kind"] == "oracle" and r["cores"] == 2 and r["value"] > 0
     assert set(r["per_type_queries_per_s"]) == {"1p", "2p"}
-    # the batch alone takes milliseconds: later query ids extend the sample
+    # later query ids extend the sample past the batch
     counts = [int(x) for x in re.findall(r": first (\d+)", r["sample"])]
     assert len(counts) == 2 and all(n > cfg.batch for n in counts)
