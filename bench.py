@@ -803,26 +803,21 @@ def main():
          for e in evl]))
     # The concurrent schedule's timed steps record only the events around one
     # kernel, the one whose roofline the line reports: the longest first-round
-    # candidate or long-list kernel of the warm-up steps, which record every
-    # event.  The other kernels' durations come from an instrumented pass of
-    # as many steps after the timed region.  The chained and split schedules
+    # candidate or long-list kernel of an instrumented pass of as many steps
+    # between the warm-up and the timed steps, which records every event and
+    # gives the other kernels' durations.  The chained and split schedules
     # need their events (the chain waits on them), so their timed steps
-    # record all of them, as does a run without warm-up steps.
-    slim = args.concurrent and not args.split and args.warmup > 0
+    # record all of them.
+    slim = args.concurrent and not args.split
     n_instr = args.steps if slim else 0
-    all_args = [step_args(k) for k in range(args.warmup + args.steps + n_instr)]
+    first_timed = args.warmup + n_instr
+    all_args = [step_args(k) for k in range(first_timed + args.steps)]
     warm = new_events(args.warmup)
     fork()
     for k in range(args.warmup):
         step(warm[k], all_args[k], k)
     merge()
     torch.cuda.synchronize()
-    only = None
-    if slim:
-        wsteps = warm[1:] if len(warm) > 1 else warm      # the first warms the shapes up
-        only = max(((qt, kind) for qt in types for kind in ("cand", "heavy")),
-                   key=lambda x: kernel_ms(wsteps, *x))
-        log(f"timed steps record the events of {only} only")
 
     def timed(first, n, restrict):
         evl = new_events(n)
@@ -845,12 +840,22 @@ def main():
         torch.cuda.synchronize()
         return evl, t_start.elapsed_time(t_end) / n, host
 
-    evs, ms_step, host_ms = timed(args.warmup, args.steps, only)
+    # the instrumented steps: every event recorded, on their own query ids
+    only, ms_instr = None, None
+    if slim:
+        evs_instr, ms_instr, _ = timed(args.warmup, n_instr, None)
+        only = max(((qt, kind) for qt in types for kind in ("cand", "heavy")),
+                   key=lambda x: kernel_ms(evs_instr, *x))
+        log(f"instrumented pass: {ms_instr:.3f} ms per step; the timed steps record the events "
+            f"of {only} only")
+
+    evs_timed, ms_step, host_ms = timed(first_timed, args.steps, only)
+    evs = evs_instr if slim else evs_timed
     log(f"host enqueue {host_ms:.3f} ms per step, device {ms_step:.3f} ms per step")
     # the schedule must not change a row: the last timed step's outputs
     # against one plain call per shape on the timing stream
-    last = all_args[args.warmup + args.steps - 1]
-    outs = outs_p[(args.warmup + args.steps - 1) % P]
+    last = all_args[first_timed + args.steps - 1]
+    outs = outs_p[(first_timed + args.steps - 1) % P]
     for qt in types:
         ref = sm.alloc_outputs(B, cfg.n_neg)
         sm.sample_positives(g, dags[qt], last[qt], ref, stream)
@@ -862,20 +867,13 @@ def main():
         del ref
     log("schedule check: every shape's rows equal those of a plain call")
 
-    # the instrumented steps: every event recorded, on new query ids
-    evs_timed = evs
-    ms_instr = None
-    if slim:
-        evs, ms_instr, _ = timed(args.warmup + args.steps, n_instr, None)
-        log(f"instrumented pass: {ms_instr:.3f} ms per step")
-
     # each shape alone (one stream, nothing else running), on new query ids:
     # per-shape rates and kernel durations without the other shapes' work
     isolated = {}
     for i, qt in enumerate(types):
         rows = []
         for k in range(args.isolated_steps):
-            off = (args.warmup + args.steps + n_instr + i * args.isolated_steps + k) * B
+            off = (first_timed + args.steps + i * args.isolated_steps + k) * B
             a = sm.make_args(B, cfg.n_neg, seed=cfg.seed, neg_tries=neg_tries, query_offset=off)
             e = [torch.cuda.Event(enable_timing=True) for _ in range(8)]
             e[0].record(stream)
@@ -973,8 +971,8 @@ def main():
     else:
         roofline = kernel_roofline(*only, ms=kernel_ms(evs_timed, *only))
         roofline["events"] = ("timed steps, which record the events around this kernel only (the "
-                              "longest of the warm-up steps); the kernels list comes from an "
-                              "instrumented pass of as many steps that records every event")
+                              "longest in the kernels list, which comes from an instrumented pass "
+                              "of as many steps before the timed ones that records every event)")
     roofline["accounting"] = (
         "achieved = algorithmic bytes / avg_launch_ms; algorithmic bytes = 64 x the distinct 64-byte "
         "lines per query that the oracle's bidirectional check under the strict node cut reads for "
